@@ -1,0 +1,231 @@
+/*
+ * wd.h - C ABI of the MI355X windowed-denoising library (libwd.so).
+ *
+ * The library runs Window-Diffusion inference (arXiv 2601.20332) of a masked
+ * diffusion language model on one AMD Instinct MI355X (gfx950): phases of one
+ * refresh step plus normal steps, an external window that keeps the first E
+ * undecoded positions (far-field positions are pruned), an internal window of
+ * active positions that alone get logits, and a per-layer K/V cache that the
+ * refresh step rewrites and normal steps reuse (Secs. 4.1-4.3 of the paper).
+ * The standard full-sequence decoding step it accelerates (Sec. 3.1) is also
+ * exported, for comparison.
+ *
+ * Conventions
+ *  - Every function returns a wd_status (or a size); no exception crosses the
+ *    ABI.  On a non-OK status wd_last_error() holds a message (per thread).
+ *  - Device memory comes from the caller: packed weights (wd_model_bytes) and
+ *    the per-generation workspace (wd_seq_bytes) are caller-allocated device
+ *    buffers, 256-byte aligned, that the caller keeps alive until the
+ *    corresponding wd_free_* call.  The library itself allocates only small
+ *    host structures and pinned host staging buffers.
+ *  - All work is enqueued on the HIP stream given to wd_init_model and is
+ *    asynchronous, except calls documented as synchronizing.
+ *  - Host arrays passed in are copied before the call returns; the caller
+ *    keeps their ownership.
+ *  - Positions are 0-based indices into one sequence (prompt first, then the
+ *    generation region).  A batch is a set of independent sequences that
+ *    step together; prompts are passed concatenated, without padding.
+ */
+#ifndef WD_H
+#define WD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WD_OK = 0,
+  WD_ERR_INVALID_ARG = -1,   /* a NULL pointer, a size out of range, a bad shape */
+  WD_ERR_OUT_OF_MEMORY = -2, /* a caller buffer is too small, or host allocation failed */
+  WD_ERR_DEVICE = -3,        /* a HIP call failed */
+  WD_ERR_STATE = -4,         /* the call is not valid in the object's current state */
+  WD_ERR_UNSUPPORTED = -5    /* a shape or setting the kernels do not implement */
+} wd_status;
+
+enum { WD_DTYPE_F32 = 0, WD_DTYPE_BF16 = 1 };
+
+/* Bidirectional decoder of the LLaDA / Qwen2 kind: pre-RMSNorm, Q/K/V
+ * projections (optional bias), RoPE (half-rotation pairs (i, i + d/2),
+ * frequency rope_theta^(-2i/d)) at absolute positions, non-causal attention
+ * with grouped K/V heads (query head h reads K/V head h / (n_heads /
+ * n_kv_heads)), output projection, SwiGLU FFN, final RMSNorm, untied LM head.
+ * dtype WD_DTYPE_BF16: bf16 weights, fp32 accumulation, fp32 residual stream;
+ * the RMSNorm outputs, Q/K after RoPE, V, the attention output and the SwiGLU
+ * product are stored as bf16 (round to nearest even).  WD_DTYPE_F32: all fp32.
+ * Supported: head_dim 64 or 128; n_heads a multiple of n_kv_heads; hidden,
+ * n_heads*head_dim, ffn and vocab multiples of 64. */
+typedef struct {
+  int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
+  int32_t mask_id;   /* the [MASK] token; never chosen as a prediction */
+  int32_t dtype;     /* WD_DTYPE_F32 or WD_DTYPE_BF16 */
+  int32_t qkv_bias;  /* 0 or 1 */
+  float rms_eps;
+  float rope_theta;
+} wd_model_config;
+
+/* Window settings (Sec. 4.2, Sec. 4.3): the internal window holds n_active
+ * positions, the external window E = n_active + n_buffer positions; a phase
+ * is refresh_every steps (one refresh step, then normal steps); each step
+ * decodes unmask_per_step positions. */
+typedef struct {
+  int32_t n_active, n_buffer, refresh_every, unmask_per_step;
+} wd_window_config;
+
+typedef struct wd_model wd_model; /* opaque: packed weights and model shape */
+typedef struct wd_seq wd_seq;     /* opaque: one batch of sequences being decoded */
+
+/* Host-side result of one step.  positions / tokens / conf point to
+ * caller-owned host arrays of batch * unmask_per_step entries; for sequence b
+ * entries [b*k, b*k + n_selected) hold the decoded positions in rank order
+ * (highest confidence first), the tokens written there and their confidence.
+ * Unused entries are set to -1 / -1 / 0. */
+typedef struct {
+  int32_t step;        /* index t of the step just taken (0-based) */
+  int32_t is_refresh;  /* 1 if it was the refresh step of a phase */
+  int32_t n_rows;      /* rows run through the layer stack, summed over the batch */
+  int32_t n_selected;  /* positions decoded per sequence in this step */
+  int32_t* positions;
+  int32_t* tokens;
+  float* conf;
+} wd_step_out;
+
+/* ---- model ------------------------------------------------------------------ */
+
+/* Number of weight tensors wd_init_model expects, in this order:
+ *   emb [vocab, hidden];
+ *   per layer: attn_norm [hidden], wq [n_heads*head_dim, hidden],
+ *     wk [n_kv_heads*head_dim, hidden], wv [n_kv_heads*head_dim, hidden],
+ *     (bq [n_heads*head_dim], bk [n_kv_heads*head_dim], bv [n_kv_heads*head_dim]
+ *      when qkv_bias), wo [hidden, n_heads*head_dim], ffn_norm [hidden],
+ *     wg [ffn, hidden], wu [ffn, hidden], wd [hidden, ffn];
+ *   final_norm [hidden]; lm_head [vocab, hidden].
+ * Matrices are row-major [out_features, in_features].  Returns -1 for an
+ * invalid or unsupported configuration. */
+int32_t wd_weight_count(const wd_model_config* cfg);
+
+/* Shape of tensor i (rows, cols; cols = 1 for vectors).  WD_ERR_INVALID_ARG
+ * for i out of range. */
+wd_status wd_weight_shape(const wd_model_config* cfg, int32_t i, int64_t* rows, int64_t* cols);
+
+/* Bytes of device memory wd_init_model needs for the packed weights; 0 for an
+ * invalid or unsupported configuration. */
+size_t wd_model_bytes(const wd_model_config* cfg);
+
+/* Packs the weights into `device_buf` (caller-owned, >= wd_model_bytes) in
+ * the layouts the kernels read.  `weights` holds wd_weight_count device
+ * pointers, each to a tensor of the model dtype (fp32, or bf16 as uint16 bit
+ * patterns) in the order above; they are only read during this call, and
+ * the caller may free them once the stream has passed it.  `stream` is a
+ * hipStream_t (NULL = the null stream) that every later call of this model
+ * and its sequences is enqueued on.  Errors: WD_ERR_INVALID_ARG (NULL
+ * pointer, n_weights mismatch), WD_ERR_UNSUPPORTED (shape), WD_ERR_OUT_OF_MEMORY
+ * (buffer too small), WD_ERR_DEVICE. */
+wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, int32_t n_weights,
+                        void* device_buf, size_t buf_bytes, void* stream, wd_model** out);
+
+void wd_free_model(wd_model* m); /* NULL is a no-op; sequences must be freed first */
+
+/* ---- one generation --------------------------------------------------------- */
+
+/* Bytes of device workspace a batch needs: token state, the K/V cache of
+ * every layer for all batch positions, activations and step buffers.
+ * 0 on invalid arguments. */
+size_t wd_seq_bytes(const wd_model* m, const wd_window_config* win, int32_t batch,
+                    const int32_t* prompt_lens, int32_t gen_len);
+
+/* Starts a generation (Sec. 3.1 initial state): sequence b is its prompt
+ * (prompt_lens[b] ids taken in order from the concatenated host array
+ * prompt_ids) followed by gen_len [MASK] tokens; prompt positions count as
+ * decoded.  Then runs the first phase's slide and refresh (wd_slide_window,
+ * wd_refresh_buffer), so the next wd_step is step 0, the phase's refresh
+ * step.  `workspace` is caller-owned device memory of >= wd_seq_bytes bytes.
+ * Errors: WD_ERR_INVALID_ARG (ids outside [0, vocab), NULL pointers,
+ * batch < 1, gen_len < 1, n_active < 1, n_buffer < 0, refresh_every < 1,
+ * unmask_per_step < 1), WD_ERR_OUT_OF_MEMORY (workspace too small),
+ * WD_ERR_DEVICE. */
+wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_t* prompt_lens,
+                            int32_t batch, int32_t gen_len, const wd_window_config* win,
+                            void* workspace, size_t ws_bytes, wd_seq** out);
+
+/* Phase start (Sec. 4.2): re-determines each sequence's external window as
+ * its first E undecoded positions, the retained prefix [0, c) (c = the E-th
+ * undecoded position + 1, or the sequence length when fewer remain) and
+ * empties the set of positions decoded in the phase.  The next step becomes
+ * the phase's refresh step.  wd_step calls it by itself when a phase is due
+ * (every refresh_every steps, or when a window has no undecoded position
+ * left); calling it earlier starts a phase early.  WD_ERR_STATE once every
+ * position is decoded, or on a sequence driven by wd_full_step. */
+wd_status wd_slide_window(wd_seq* s);
+
+/* Refresh (Sec. 4.3, refresh equation): a full forward over each sequence's
+ * retained prefix [0, c) that rewrites the K/V cache rows of every layer and
+ * keeps the active rows' final hidden states for the refresh step's logits.
+ * Requires a slid phase whose refresh step has not been taken
+ * (WD_ERR_STATE otherwise). */
+wd_status wd_refresh_buffer(wd_seq* s);
+
+/* One diffusion step.  If a phase is due it slides and refreshes first.  On
+ * the refresh step the active rows' logits come from the refresh forward; on
+ * a normal step only the online rows (active positions and positions decoded
+ * earlier in the phase) run the layer stack, overwrite their own K/V rows and
+ * attend to all cached rows of [0, c).  Then logits on the active positions,
+ * confidence (softmax probability of the argmax token, [MASK] excluded, ties
+ * to the lowest id) and the unmask_per_step most confident positions are
+ * decoded (ties to the lowest position).  `out` may be NULL (fully
+ * asynchronous); otherwise the call synchronizes the stream and fills it.
+ * WD_ERR_STATE when every position is already decoded. */
+wd_status wd_step(wd_seq* s, wd_step_out* out);
+
+/* Standard decoding step (Sec. 3.1) for comparison: a forward over every
+ * position of every sequence, logits for every undecoded position, and the
+ * unmask_per_step most confident of them decoded.  A sequence is driven
+ * either by wd_full_step or by the windowed calls, never both
+ * (WD_ERR_STATE). */
+wd_status wd_full_step(wd_seq* s, wd_step_out* out);
+
+/* Synchronizes, then copies the token ids (sum of sequence lengths, sequence
+ * after sequence) and the step counter to the host.  `decoded` (same length,
+ * 1 = decoded) may be NULL. */
+wd_status wd_get_state(const wd_seq* s, int32_t* tokens, uint8_t* decoded, int32_t* t);
+
+/* Synchronizes, then copies the last step's active-row logits (fp32,
+ * [n_rows, vocab], sequence after sequence, active positions in increasing
+ * order) and, when `positions` is not NULL, those rows' positions; *n_rows
+ * receives the row count.  `capacity` is the number of rows the caller's
+ * arrays hold (WD_ERR_OUT_OF_MEMORY if too small).  For tests. */
+wd_status wd_debug_logits(const wd_seq* s, float* logits, int32_t* positions, int32_t capacity,
+                          int32_t* n_rows);
+
+/* Synchronizes, then copies K and V of one layer and one sequence for
+ * positions [0, c) as fp32 [c, n_kv_heads, head_dim] each, with c the
+ * current retained prefix; *ctx_len receives c.  `capacity` is the number of
+ * positions the arrays hold.  For tests. */
+wd_status wd_debug_kv(const wd_seq* s, int32_t layer, int32_t b, float* k, float* v,
+                      int32_t capacity, int32_t* ctx_len);
+
+void wd_free_seq(wd_seq* s); /* NULL is a no-op; synchronizes the stream */
+
+/* ---- host-only helpers -------------------------------------------------------- */
+
+/* The schedule's counts for one sequence, from counts alone (they do not
+ * depend on which positions get decoded): for each step t, whether it is a
+ * refresh step, the retained prefix length c, |A|, the rows the step runs
+ * through the layer stack (c on a refresh step, |A| + |D_p| otherwise) and
+ * the positions it decodes.  Writes at most max_steps entries to each
+ * non-NULL array and returns the total number of steps, or -1 on invalid
+ * arguments.  Needs no GPU. */
+int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, int32_t max_steps,
+                int32_t* is_refresh, int32_t* ctx_len, int32_t* n_active, int32_t* n_rows,
+                int32_t* n_decode);
+
+/* Message of the last non-OK status on this thread ("" if none). */
+const char* wd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WD_H */

@@ -1,0 +1,979 @@
+// libwd host runtime: the C ABI of include/wd.h.
+//
+// The host keeps the schedule's counts (they do not depend on which positions
+// get decoded, so every launch size is known without reading the device);
+// the device keeps the token state and derives the identities of the rows
+// (build_rows) from the decoded flags.  Nothing is read back between steps
+// unless the caller asks for a step's result.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/wd.h"
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+wd_status fail(wd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define WD_HIP(call)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (call);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(WD_ERR_DEVICE, "%s failed: %s", #call, hipGetErrorString(e_));       \
+  } while (0)
+
+#define WD_TRY(call)                   \
+  do {                                 \
+    wd_status s_ = (call);             \
+    if (s_ != WD_OK) return s_;        \
+  } while (0)
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// -- model shape checks --------------------------------------------------------------
+bool cfg_valid(const wd_model_config* c, std::string* why) {
+  if (!c) {
+    *why = "NULL config";
+    return false;
+  }
+  if (c->n_layers < 1 || c->hidden < 64 || c->n_heads < 1 || c->n_kv_heads < 1 || c->vocab < 2 ||
+      c->ffn < 64) {
+    *why = "non-positive or too small dimension";
+    return false;
+  }
+  if (c->dtype != WD_DTYPE_F32 && c->dtype != WD_DTYPE_BF16) {
+    *why = "dtype must be WD_DTYPE_F32 or WD_DTYPE_BF16";
+    return false;
+  }
+  if (c->head_dim != 64 && c->head_dim != 128) {
+    *why = "head_dim must be 64 or 128";
+    return false;
+  }
+  if (c->dtype == WD_DTYPE_BF16 && c->head_dim != 128) {
+    *why = "bf16 models need head_dim 128";
+    return false;
+  }
+  if (c->n_heads % c->n_kv_heads) {
+    *why = "n_heads must be a multiple of n_kv_heads";
+    return false;
+  }
+  if (c->hidden % 64 || (c->n_heads * c->head_dim) % 64 || c->ffn % 64 || c->vocab % 64) {
+    *why = "hidden, n_heads*head_dim, ffn and vocab must be multiples of 64";
+    return false;
+  }
+  if (c->mask_id < 0 || c->mask_id >= c->vocab) {
+    *why = "mask_id outside [0, vocab)";
+    return false;
+  }
+  if (c->qkv_bias != 0 && c->qkv_bias != 1) {
+    *why = "qkv_bias must be 0 or 1";
+    return false;
+  }
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f)) {
+    *why = "rms_eps must be > 0 and rope_theta > 1";
+    return false;
+  }
+  return true;
+}
+
+struct TensorSpec {
+  long rows, cols;
+};
+
+std::vector<TensorSpec> tensor_specs(const wd_model_config& c) {
+  const long H = c.hidden, Q = (long)c.n_heads * c.head_dim, KV = (long)c.n_kv_heads * c.head_dim;
+  std::vector<TensorSpec> v;
+  v.push_back({c.vocab, H});
+  for (int l = 0; l < c.n_layers; ++l) {
+    v.push_back({H, 1});
+    v.push_back({Q, H});
+    v.push_back({KV, H});
+    v.push_back({KV, H});
+    if (c.qkv_bias) {
+      v.push_back({Q, 1});
+      v.push_back({KV, 1});
+      v.push_back({KV, 1});
+    }
+    v.push_back({H, Q});
+    v.push_back({H, 1});
+    v.push_back({c.ffn, H});
+    v.push_back({c.ffn, H});
+    v.push_back({H, c.ffn});
+  }
+  v.push_back({H, 1});
+  v.push_back({c.vocab, H});
+  return v;
+}
+
+// -- the schedule's counts (shared by the runtime and wd_plan) ---------------------
+struct Counts {
+  int E = 0, R = 1, k = 1, na = 1;
+  int u = 0;          // undecoded positions per sequence
+  int in_window = 0;  // undecoded positions of the current window
+  int dp = 0;         // positions decoded in the current phase
+  int j = -1;         // steps taken in the current phase (-1: no phase yet)
+
+  bool phase_due() const { return j < 0 || j >= R || in_window == 0; }
+  int ctx(int S) const { return u >= E ? S - u + E : S; }
+  void start_phase() {
+    in_window = std::min(E, u);
+    dp = 0;
+    j = 0;
+  }
+  int n_active() const { return std::min(na, in_window); }
+  int n_decode() const { return std::min(k, n_active()); }
+  void take_step() {
+    const int d = n_decode();
+    u -= d;
+    in_window -= d;
+    dp += d;
+    ++j;
+  }
+};
+
+}  // namespace
+
+// -- model ---------------------------------------------------------------------------
+struct LayerW {
+  const void* attn_norm;
+  const void* wqkv;
+  const void* bqkv;  // NULL without bias
+  const void* wo;
+  const void* ffn_norm;
+  const void* wgu;
+  const void* wd;
+};
+
+struct wd_model {
+  wd_model_config cfg;
+  hipStream_t stream;
+  int device;
+  size_t esz;
+  int qkv_n;
+  const void* emb;
+  const void* final_norm;
+  const void* lm;
+  std::vector<LayerW> layers;
+  int live_seqs = 0;
+};
+
+namespace {
+
+// Byte layout of the packed weight buffer; the same walk sizes and fills it.
+struct ModelLayout {
+  size_t total = 0;
+  size_t emb, final_norm, lm;
+  struct L {
+    size_t attn_norm, wqkv, bqkv, wo, ffn_norm, wgu, wd;
+  };
+  std::vector<L> layers;
+};
+
+ModelLayout model_layout(const wd_model_config& c) {
+  const size_t e = c.dtype == WD_DTYPE_BF16 ? 2 : 4;
+  const size_t H = c.hidden, Q = (size_t)c.n_heads * c.head_dim,
+               KV = (size_t)c.n_kv_heads * c.head_dim, F = c.ffn;
+  ModelLayout m;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += align256(bytes);
+    return at;
+  };
+  m.emb = take((size_t)c.vocab * H * e);
+  for (int l = 0; l < c.n_layers; ++l) {
+    ModelLayout::L L;
+    L.attn_norm = take(H * e);
+    L.wqkv = take((Q + 2 * KV) * H * e);
+    L.bqkv = c.qkv_bias ? take((Q + 2 * KV) * e) : 0;
+    L.wo = take(H * Q * e);
+    L.ffn_norm = take(H * e);
+    L.wgu = take(2 * F * H * e);
+    L.wd = take(H * F * e);
+    m.layers.push_back(L);
+  }
+  m.final_norm = take(H * e);
+  m.lm = take((size_t)c.vocab * H * e);
+  m.total = o;
+  return m;
+}
+
+// Copies (fp32) or packs into MFMA fragments (bf16) one [N, K] matrix at dst.
+wd_status put_matrix(const wd_model& m, const void* src, long N, long K, char* dst) {
+  if (m.cfg.dtype == WD_DTYPE_BF16) {
+    WD_HIP(wd::pack_frags((const uint16_t*)src, (int)N, (int)K, dst, m.stream));
+  } else {
+    WD_HIP(hipMemcpyAsync(dst, src, (size_t)N * K * 4, hipMemcpyDeviceToDevice, m.stream));
+  }
+  return WD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* wd_last_error(void) { return g_err.c_str(); }
+
+int32_t wd_weight_count(const wd_model_config* cfg) {
+  std::string why;
+  if (!cfg_valid(cfg, &why)) return -1;
+  return (int32_t)tensor_specs(*cfg).size();
+}
+
+wd_status wd_weight_shape(const wd_model_config* cfg, int32_t i, int64_t* rows, int64_t* cols) {
+  std::string why;
+  if (!cfg_valid(cfg, &why)) return fail(WD_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
+  const auto v = tensor_specs(*cfg);
+  if (i < 0 || i >= (int32_t)v.size() || !rows || !cols)
+    return fail(WD_ERR_INVALID_ARG, "tensor index %d out of range", i);
+  *rows = v[i].rows;
+  *cols = v[i].cols;
+  return WD_OK;
+}
+
+size_t wd_model_bytes(const wd_model_config* cfg) {
+  std::string why;
+  if (!cfg_valid(cfg, &why)) return 0;
+  return model_layout(*cfg).total;
+}
+
+wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, int32_t n_weights,
+                        void* device_buf, size_t buf_bytes, void* stream, wd_model** out) {
+  std::string why;
+  if (!out) return fail(WD_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!cfg_valid(cfg, &why)) {
+    const bool shape = cfg && why.find("NULL") == std::string::npos &&
+                       why.find("non-positive") == std::string::npos;
+    return fail(shape ? WD_ERR_UNSUPPORTED : WD_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
+  }
+  const auto specs = tensor_specs(*cfg);
+  if (!weights || n_weights != (int32_t)specs.size())
+    return fail(WD_ERR_INVALID_ARG, "expected %zu weight pointers, got %d", specs.size(), n_weights);
+  for (size_t i = 0; i < specs.size(); ++i) {
+    if (!weights[i]) return fail(WD_ERR_INVALID_ARG, "weight %zu is NULL", i);
+    if (((uintptr_t)weights[i]) & 15)
+      return fail(WD_ERR_INVALID_ARG, "weight %zu is not 16-byte aligned", i);
+  }
+  const ModelLayout lay = model_layout(*cfg);
+  if (!device_buf) return fail(WD_ERR_INVALID_ARG, "device_buf is NULL");
+  if (((uintptr_t)device_buf) & 255) return fail(WD_ERR_INVALID_ARG, "device_buf not 256-byte aligned");
+  if (buf_bytes < lay.total)
+    return fail(WD_ERR_OUT_OF_MEMORY, "device_buf holds %zu bytes, %zu needed", buf_bytes, lay.total);
+
+  wd_model* m = new (std::nothrow) wd_model();
+  if (!m) return fail(WD_ERR_OUT_OF_MEMORY, "host allocation failed");
+  m->cfg = *cfg;
+  m->stream = (hipStream_t)stream;
+  if (hipGetDevice(&m->device) != hipSuccess) {
+    delete m;
+    return fail(WD_ERR_DEVICE, "hipGetDevice failed");
+  }
+  m->esz = cfg->dtype == WD_DTYPE_BF16 ? 2 : 4;
+  m->qkv_n = (cfg->n_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
+  char* base = (char*)device_buf;
+  const long H = cfg->hidden, Q = (long)cfg->n_heads * cfg->head_dim,
+             KV = (long)cfg->n_kv_heads * cfg->head_dim, F = cfg->ffn;
+  const size_t e = m->esz;
+  auto fail_free = [&](wd_status s) {
+    delete m;
+    return s;
+  };
+  auto copy = [&](const void* src, size_t bytes, char* dst) -> wd_status {
+    WD_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, m->stream));
+    return WD_OK;
+  };
+  // packed size of an [N, K] matrix (fragments are exactly N*K elements)
+  size_t wi = 0;
+  wd_status st;
+  if ((st = copy(weights[wi++], (size_t)cfg->vocab * H * e, base + lay.emb)) != WD_OK) return fail_free(st);
+  m->emb = base + lay.emb;
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const auto& L = lay.layers[l];
+    LayerW w{};
+    if ((st = copy(weights[wi++], H * e, base + L.attn_norm)) != WD_OK) return fail_free(st);
+    const void* wq = weights[wi++];
+    const void* wk = weights[wi++];
+    const void* wv = weights[wi++];
+    if ((st = put_matrix(*m, wq, Q, H, base + L.wqkv)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, wk, KV, H, base + L.wqkv + Q * H * e)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, wv, KV, H, base + L.wqkv + (Q + KV) * H * e)) != WD_OK) return fail_free(st);
+    if (cfg->qkv_bias) {
+      if ((st = copy(weights[wi++], Q * e, base + L.bqkv)) != WD_OK) return fail_free(st);
+      if ((st = copy(weights[wi++], KV * e, base + L.bqkv + Q * e)) != WD_OK) return fail_free(st);
+      if ((st = copy(weights[wi++], KV * e, base + L.bqkv + (Q + KV) * e)) != WD_OK) return fail_free(st);
+      w.bqkv = base + L.bqkv;
+    }
+    if ((st = put_matrix(*m, weights[wi++], H, Q, base + L.wo)) != WD_OK) return fail_free(st);
+    if ((st = copy(weights[wi++], H * e, base + L.ffn_norm)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, weights[wi++], F, H, base + L.wgu)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, weights[wi++], F, H, base + L.wgu + F * H * e)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, weights[wi++], H, F, base + L.wd)) != WD_OK) return fail_free(st);
+    w.attn_norm = base + L.attn_norm;
+    w.wqkv = base + L.wqkv;
+    w.wo = base + L.wo;
+    w.ffn_norm = base + L.ffn_norm;
+    w.wgu = base + L.wgu;
+    w.wd = base + L.wd;
+    m->layers.push_back(w);
+  }
+  if ((st = copy(weights[wi++], H * e, base + lay.final_norm)) != WD_OK) return fail_free(st);
+  m->final_norm = base + lay.final_norm;
+  if ((st = put_matrix(*m, weights[wi++], cfg->vocab, H, base + lay.lm)) != WD_OK) return fail_free(st);
+  m->lm = base + lay.lm;
+  if (hipStreamSynchronize(m->stream) != hipSuccess) {
+    delete m;
+    return fail(WD_ERR_DEVICE, "weight packing failed");
+  }
+  *out = m;
+  return WD_OK;
+}
+
+void wd_free_model(wd_model* m) { delete m; }
+
+}  // extern "C"
+
+// -- one generation -----------------------------------------------------------------------
+struct wd_seq {
+  wd_model* m = nullptr;
+  wd_window_config win{};
+  int B = 0, G = 0;
+  long T = 0;
+  int Smax = 0;
+  std::vector<int> np, S, off, ctx;
+  Counts cnt;
+  int t = 0;
+  bool refreshed = false;
+  int mode = 0;  // 0 = not started, 1 = windowed, 2 = full sequence
+  int last_nA = 0;
+  // device buffers (carved from the caller's workspace)
+  int32_t *x, *seq_len, *row_tok, *row_pos, *row_seq, *row_out, *act_pos, *act_tok, *sel_pos,
+      *sel_tok, *err;
+  uint8_t *dec, *dec0;
+  float *rope, *h, *C, *logits, *act_conf, *sel_conf, *dbg;
+  void *kc, *vc, *a, *q, *o, *sw, *a_act;
+  long M_max = 0, A_max = 0;
+  size_t C_floats = 0;
+  // pinned host staging for step results
+  int32_t* h_buf = nullptr;
+};
+
+namespace {
+
+struct SeqLayout {
+  size_t total = 0;
+  size_t x, seq_len, dec, dec0, kc, vc, rope, h, a, q, o, sw, C, row_tok, row_pos, row_seq, row_out,
+      act_pos, act_tok, act_conf, a_act, logits, sel_pos, sel_tok, sel_conf, err, dbg;
+  long M_max, A_max;
+  size_t C_floats;
+};
+
+int gemm_splits(const wd_model_config& c, int M, int N, int K) {
+  if (c.dtype != WD_DTYPE_BF16) return 1;
+  return wd::plan_gemm_bf16(M, N, K).splits;
+}
+
+SeqLayout seq_layout(const wd_model& m, const wd_window_config& w, int B, long T, int Smax, int G) {
+  const wd_model_config& c = m.cfg;
+  const size_t e = m.esz;
+  const long H = c.hidden, Q = (long)c.n_heads * c.head_dim, KVd = (long)c.n_kv_heads * c.head_dim,
+             F = c.ffn;
+  SeqLayout s;
+  s.M_max = T;
+  s.A_max = std::max<long>((long)B * w.n_active, (long)B * G);
+  size_t cf = 0;
+  const int shapes[4][2] = {{m.qkv_n, (int)H}, {(int)H, (int)Q}, {(int)(2 * F), (int)H}, {(int)H, (int)F}};
+  for (long M = 1; M <= s.M_max; ++M)
+    for (auto& sh : shapes) cf = std::max(cf, (size_t)gemm_splits(c, (int)M, sh[0], sh[1]) * M * sh[0]);
+  s.C_floats = cf;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += align256(bytes);
+    return at;
+  };
+  s.x = take(T * 4);
+  s.seq_len = take(B * 4);
+  s.dec = take(T);
+  s.dec0 = take(T);
+  s.kc = take((size_t)c.n_layers * KVd * T * e);
+  s.vc = take((size_t)c.n_layers * KVd * T * e);
+  s.rope = take((size_t)Smax * c.head_dim * 4);
+  s.h = take(s.M_max * H * 4);
+  s.a = take(s.M_max * H * e);
+  s.q = take(s.M_max * Q * e);
+  s.o = take(s.M_max * Q * e);
+  s.sw = take(s.M_max * F * e);
+  s.C = take(cf * 4);
+  s.row_tok = take(s.M_max * 4);
+  s.row_pos = take(s.M_max * 4);
+  s.row_seq = take(s.M_max * 4);
+  s.row_out = take(s.M_max * 4);
+  s.act_pos = take(s.A_max * 4);
+  s.act_tok = take(s.A_max * 4);
+  s.act_conf = take(s.A_max * 4);
+  s.a_act = take(s.A_max * H * e);
+  s.logits = take((size_t)s.A_max * c.vocab * 4);
+  s.sel_pos = take((size_t)B * w.unmask_per_step * 4);
+  s.sel_tok = take((size_t)B * w.unmask_per_step * 4);
+  s.sel_conf = take((size_t)B * w.unmask_per_step * 4);
+  s.err = take(4);
+  s.dbg = take((size_t)T * c.head_dim * 4);
+  s.total = o;
+  return s;
+}
+
+bool win_valid(const wd_window_config* w, std::string* why) {
+  if (!w) {
+    *why = "NULL window config";
+    return false;
+  }
+  if (w->n_active < 1 || w->n_buffer < 0 || w->refresh_every < 1 || w->unmask_per_step < 1) {
+    *why = "need n_active >= 1, n_buffer >= 0, refresh_every >= 1, unmask_per_step >= 1";
+    return false;
+  }
+  if (w->n_active > 64) {
+    *why = "n_active above 64 is not supported";
+    return false;
+  }
+  return true;
+}
+
+bool seq_args_valid(const wd_model* m, const wd_window_config* w, int32_t batch,
+                    const int32_t* prompt_lens, int32_t gen_len, std::string* why) {
+  if (!m) {
+    *why = "model is NULL";
+    return false;
+  }
+  if (!win_valid(w, why)) return false;
+  if (batch < 1 || batch > WD_MAX_BATCH) {
+    *why = "batch must be in [1, 64]";
+    return false;
+  }
+  if (!prompt_lens) {
+    *why = "prompt_lens is NULL";
+    return false;
+  }
+  if (gen_len < 1) {
+    *why = "gen_len must be >= 1";
+    return false;
+  }
+  long T = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (prompt_lens[b] < 0) {
+      *why = "negative prompt length";
+      return false;
+    }
+    T += prompt_lens[b] + gen_len;
+  }
+  if (T > (1L << 24)) {
+    *why = "too many positions";
+    return false;
+  }
+  if (m->cfg.dtype == WD_DTYPE_F32) {
+    for (int b = 0; b < batch; ++b)
+      if (prompt_lens[b] + gen_len > 16384) {
+        *why = "fp32 models support sequences of at most 16384 positions";
+        return false;
+      }
+  }
+  return true;
+}
+
+// ---- the layer stack over a row set ----------------------------------------------------------
+struct Rows {
+  int M;
+  int n_act;  // active rows per sequence (compact index b * n_act + rank)
+  WdStepGeom g;
+};
+
+template <typename T>
+wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
+               int max_splits, int* splits) {
+  const wd_model& m = *s->m;
+  if (m.cfg.dtype == WD_DTYPE_BF16) {
+    wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K);
+    if (p.splits > max_splits) {
+      p.splits = 1;
+      p.ks_per_split = K / 32;
+      p.grid = (N / 32) * ((M + 63) / 64);
+    }
+    if ((size_t)p.splits * M * N > s->C_floats && C == s->C)
+      return fail(WD_ERR_DEVICE, "internal: partial buffer too small");
+    WD_HIP(wd::gemm_bf16((const uint16_t*)X, ldx, W, C, M, N, K, p, m.stream));
+    *splits = p.splits;
+  } else {
+    WD_HIP(wd::gemm_f32((const float*)X, ldx, (const float*)W, C, M, N, K, m.stream));
+    *splits = 1;
+  }
+  return WD_OK;
+}
+
+template <typename T>
+wd_status run_layers(wd_seq* s, const Rows& r) {
+  const wd_model& m = *s->m;
+  const wd_model_config& c = m.cfg;
+  hipStream_t st = m.stream;
+  const int M = r.M, H = c.hidden, Q = c.n_heads * c.head_dim, F = c.ffn;
+  const long KVd = (long)c.n_kv_heads * c.head_dim;
+  T* a = (T*)s->a;
+  T* q = (T*)s->q;
+  T* o = (T*)s->o;
+  T* sw = (T*)s->sw;
+  WD_HIP(wd::embed_norm<T>(s->x, s->row_tok, (const T*)m.emb, (const T*)m.layers[0].attn_norm,
+                           c.rms_eps, s->h, a, M, H, st));
+  int S;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const LayerW& w = m.layers[l];
+    T* kc = (T*)s->kc + (size_t)l * KVd * s->T;
+    T* vc = (T*)s->vc + (size_t)l * KVd * s->T;
+    WD_TRY(gemm<T>(s, a, H, w.wqkv, s->C, M, m.qkv_n, H, 1 << 20, &S));
+    WD_HIP(wd::qkv_epilogue<T>(s->C, S, M, (const T*)w.bqkv, s->rope, s->row_pos, s->row_tok,
+                               c.n_heads, c.n_kv_heads, c.head_dim, q, kc, vc, s->T, st));
+    if (c.dtype == WD_DTYPE_BF16) {
+      WD_HIP(wd::attention_bf16((const uint16_t*)q, (const uint16_t*)kc, (const uint16_t*)vc, s->T,
+                                (uint16_t*)o, r.g, c.n_heads, c.n_kv_heads, c.head_dim, st));
+    } else {
+      WD_HIP(wd::attention_f32((const float*)q, (const float*)kc, (const float*)vc, s->T,
+                               (float*)o, s->row_seq, M, r.g, c.n_heads, c.n_kv_heads, c.head_dim,
+                               st));
+    }
+    WD_TRY(gemm<T>(s, o, Q, w.wo, s->C, M, H, Q, 1 << 20, &S));
+    WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)w.ffn_norm, c.rms_eps, a, nullptr, st));
+    WD_TRY(gemm<T>(s, a, H, w.wgu, s->C, M, 2 * F, H, 1 << 20, &S));
+    WD_HIP(wd::swiglu<T>(s->C, S, M, F, sw, st));
+    WD_TRY(gemm<T>(s, sw, F, w.wd, s->C, M, H, F, 1 << 20, &S));
+    if (l + 1 < c.n_layers) {
+      WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)m.layers[l + 1].attn_norm,
+                                  c.rms_eps, a, nullptr, st));
+    } else {
+      WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)m.final_norm, c.rms_eps,
+                                  (T*)s->a_act, s->row_out, st));
+    }
+  }
+  return WD_OK;
+}
+
+wd_status forward(wd_seq* s, int mode, const Rows& r) {
+  WD_HIP(wd::build_rows(mode, s->dec, s->dec0, r.n_act, r.g, s->row_tok, s->row_pos, s->row_seq,
+                        s->row_out, s->act_pos, s->err, s->m->stream));
+  if (s->m->cfg.dtype == WD_DTYPE_BF16) return run_layers<uint16_t>(s, r);
+  return run_layers<float>(s, r);
+}
+
+WdStepGeom base_geom(const wd_seq* s) {
+  WdStepGeom g;
+  memset(&g, 0, sizeof(g));
+  g.batch = s->B;
+  for (int b = 0; b < s->B; ++b) {
+    g.off[b] = s->off[b];
+    g.ctx[b] = s->ctx.empty() ? s->S[b] : s->ctx[b];
+  }
+  return g;
+}
+
+// LM head on the compact active rows, confidence, top-k decode.
+wd_status decide(wd_seq* s, int n_act) {
+  const wd_model& m = *s->m;
+  const wd_model_config& c = m.cfg;
+  const int n = s->B * n_act;
+  int S;
+  if (c.dtype == WD_DTYPE_BF16)
+    WD_TRY(gemm<uint16_t>(s, (const uint16_t*)s->a_act, c.hidden, m.lm, s->logits, n, c.vocab,
+                          c.hidden, 1, &S));
+  else
+    WD_TRY(gemm<float>(s, (const float*)s->a_act, c.hidden, m.lm, s->logits, n, c.vocab, c.hidden,
+                       1, &S));
+  WD_HIP(wd::confidence(s->logits, n, c.vocab, c.mask_id, s->act_tok, s->act_conf, m.stream));
+  const WdStepGeom g = base_geom(s);
+  WD_HIP(wd::select_update(s->act_pos, s->act_tok, s->act_conf, n_act, s->win.unmask_per_step, g,
+                           s->seq_len, s->x, s->dec, s->sel_pos, s->sel_tok, s->sel_conf, m.stream));
+  s->last_nA = n_act;
+  return WD_OK;
+}
+
+wd_status do_slide(wd_seq* s) {
+  s->cnt.start_phase();
+  for (int b = 0; b < s->B; ++b) s->ctx[b] = s->cnt.ctx(s->S[b]);
+  s->refreshed = false;
+  const WdStepGeom g = base_geom(s);
+  WD_HIP(wd::slide(s->dec, s->dec0, s->T, s->cnt.E, g, s->seq_len, s->err, s->m->stream));
+  return WD_OK;
+}
+
+wd_status do_refresh(wd_seq* s) {
+  Rows r;
+  r.g = base_geom(s);
+  r.n_act = s->cnt.n_active();
+  int row = 0;
+  for (int b = 0; b < s->B; ++b) {
+    r.g.row0[b] = row;
+    r.g.nrows[b] = s->ctx[b];
+    row += s->ctx[b];
+  }
+  r.M = row;
+  WD_TRY(forward(s, 0, r));
+  s->refreshed = true;
+  return WD_OK;
+}
+
+wd_status do_normal(wd_seq* s) {
+  Rows r;
+  r.g = base_geom(s);
+  r.n_act = s->cnt.n_active();
+  const int nO = r.n_act + s->cnt.dp;
+  for (int b = 0; b < s->B; ++b) {
+    r.g.row0[b] = b * nO;
+    r.g.nrows[b] = nO;
+  }
+  r.M = s->B * nO;
+  return forward(s, 1, r);
+}
+
+wd_status fetch_out(wd_seq* s, wd_step_out* out, int step, int refresh, int rows, int nsel) {
+  const int k = s->win.unmask_per_step, B = s->B;
+  hipStream_t st = s->m->stream;
+  WD_HIP(hipMemcpyAsync(s->h_buf, s->sel_pos, B * k * 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipMemcpyAsync(s->h_buf + B * k, s->sel_tok, B * k * 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipMemcpyAsync(s->h_buf + 2 * B * k, s->sel_conf, B * k * 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipMemcpyAsync(s->h_buf + 3 * B * k, s->err, 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipStreamSynchronize(st));
+  if (s->h_buf[3 * B * k] != 0)
+    return fail(WD_ERR_DEVICE, "device bookkeeping disagrees with the schedule (code %d)",
+                s->h_buf[3 * B * k]);
+  out->step = step;
+  out->is_refresh = refresh;
+  out->n_rows = rows;
+  out->n_selected = nsel;
+  if (out->positions) memcpy(out->positions, s->h_buf, B * k * 4);
+  if (out->tokens) memcpy(out->tokens, s->h_buf + B * k, B * k * 4);
+  if (out->conf) memcpy(out->conf, s->h_buf + 2 * B * k, B * k * 4);
+  return WD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t wd_seq_bytes(const wd_model* m, const wd_window_config* win, int32_t batch,
+                    const int32_t* prompt_lens, int32_t gen_len) {
+  std::string why;
+  if (!seq_args_valid(m, win, batch, prompt_lens, gen_len, &why)) return 0;
+  long T = 0;
+  int Smax = 0;
+  for (int b = 0; b < batch; ++b) {
+    T += prompt_lens[b] + gen_len;
+    Smax = std::max(Smax, prompt_lens[b] + gen_len);
+  }
+  return seq_layout(*m, *win, batch, T, Smax, gen_len).total;
+}
+
+wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_t* prompt_lens,
+                            int32_t batch, int32_t gen_len, const wd_window_config* win,
+                            void* workspace, size_t ws_bytes, wd_seq** out) {
+  std::string why;
+  if (!out) return fail(WD_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!seq_args_valid(m, win, batch, prompt_lens, gen_len, &why))
+    return fail(WD_ERR_INVALID_ARG, "%s", why.c_str());
+  long n_ids = 0;
+  for (int b = 0; b < batch; ++b) n_ids += prompt_lens[b];
+  if (n_ids > 0 && !prompt_ids) return fail(WD_ERR_INVALID_ARG, "prompt_ids is NULL");
+  for (long i = 0; i < n_ids; ++i)
+    if (prompt_ids[i] < 0 || prompt_ids[i] >= m->cfg.vocab)
+      return fail(WD_ERR_INVALID_ARG, "prompt id %d at %ld outside [0, vocab)", prompt_ids[i], i);
+  if (!workspace) return fail(WD_ERR_INVALID_ARG, "workspace is NULL");
+  if (((uintptr_t)workspace) & 255) return fail(WD_ERR_INVALID_ARG, "workspace not 256-byte aligned");
+  if (hipSetDevice(m->device) != hipSuccess) return fail(WD_ERR_DEVICE, "hipSetDevice failed");
+
+  wd_seq* s = new (std::nothrow) wd_seq();
+  if (!s) return fail(WD_ERR_OUT_OF_MEMORY, "host allocation failed");
+  s->m = m;
+  s->win = *win;
+  s->B = batch;
+  s->G = gen_len;
+  long T = 0;
+  for (int b = 0; b < batch; ++b) {
+    s->np.push_back(prompt_lens[b]);
+    s->S.push_back(prompt_lens[b] + gen_len);
+    s->off.push_back((int)T);
+    T += prompt_lens[b] + gen_len;
+    s->Smax = std::max(s->Smax, prompt_lens[b] + gen_len);
+  }
+  s->T = T;
+  s->ctx.assign(batch, 0);
+  const SeqLayout L = seq_layout(*m, *win, batch, T, s->Smax, gen_len);
+  if (ws_bytes < L.total) {
+    delete s;
+    return fail(WD_ERR_OUT_OF_MEMORY, "workspace holds %zu bytes, %zu needed", ws_bytes, L.total);
+  }
+  char* base = (char*)workspace;
+  s->x = (int32_t*)(base + L.x);
+  s->seq_len = (int32_t*)(base + L.seq_len);
+  s->dec = (uint8_t*)(base + L.dec);
+  s->dec0 = (uint8_t*)(base + L.dec0);
+  s->kc = base + L.kc;
+  s->vc = base + L.vc;
+  s->rope = (float*)(base + L.rope);
+  s->h = (float*)(base + L.h);
+  s->a = base + L.a;
+  s->q = base + L.q;
+  s->o = base + L.o;
+  s->sw = base + L.sw;
+  s->C = (float*)(base + L.C);
+  s->row_tok = (int32_t*)(base + L.row_tok);
+  s->row_pos = (int32_t*)(base + L.row_pos);
+  s->row_seq = (int32_t*)(base + L.row_seq);
+  s->row_out = (int32_t*)(base + L.row_out);
+  s->act_pos = (int32_t*)(base + L.act_pos);
+  s->act_tok = (int32_t*)(base + L.act_tok);
+  s->act_conf = (float*)(base + L.act_conf);
+  s->a_act = base + L.a_act;
+  s->logits = (float*)(base + L.logits);
+  s->sel_pos = (int32_t*)(base + L.sel_pos);
+  s->sel_tok = (int32_t*)(base + L.sel_tok);
+  s->sel_conf = (float*)(base + L.sel_conf);
+  s->err = (int32_t*)(base + L.err);
+  s->dbg = (float*)(base + L.dbg);
+  s->M_max = L.M_max;
+  s->A_max = L.A_max;
+  s->C_floats = L.C_floats;
+
+  s->cnt.E = win->n_active + win->n_buffer;
+  s->cnt.R = win->refresh_every;
+  s->cnt.k = win->unmask_per_step;
+  s->cnt.na = win->n_active;
+  s->cnt.u = gen_len;
+  s->cnt.j = -1;
+
+  // host-side initial state
+  std::vector<int32_t> x(T);
+  std::vector<uint8_t> dec(T);
+  long p = 0, id = 0;
+  for (int b = 0; b < batch; ++b) {
+    for (int i = 0; i < prompt_lens[b]; ++i) {
+      x[p] = prompt_ids[id++];
+      dec[p++] = 1;
+    }
+    for (int i = 0; i < gen_len; ++i) {
+      x[p] = m->cfg.mask_id;
+      dec[p++] = 0;
+    }
+  }
+  const int half = m->cfg.head_dim / 2;
+  std::vector<float> rope((size_t)s->Smax * half * 2);
+  for (int pos = 0; pos < s->Smax; ++pos)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)pos * std::pow((double)m->cfg.rope_theta, -2.0 * i / m->cfg.head_dim);
+      rope[((size_t)pos * half + i) * 2] = (float)std::cos(ang);
+      rope[((size_t)pos * half + i) * 2 + 1] = (float)std::sin(ang);
+    }
+  const int32_t zero = 0;
+  hipStream_t st = m->stream;
+  const size_t kv_bytes = (size_t)m->cfg.n_layers * m->cfg.n_kv_heads * m->cfg.head_dim * T * m->esz;
+  bool ok = hipHostMalloc((void**)&s->h_buf, (size_t)(3 * batch * win->unmask_per_step + 1) * 4,
+                          hipHostMallocDefault) == hipSuccess;
+  ok = ok && hipMemcpyAsync(s->x, x.data(), T * 4, hipMemcpyHostToDevice, st) == hipSuccess;
+  ok = ok && hipMemcpyAsync(s->dec, dec.data(), T, hipMemcpyHostToDevice, st) == hipSuccess;
+  ok = ok && hipMemcpyAsync(s->dec0, dec.data(), T, hipMemcpyHostToDevice, st) == hipSuccess;
+  ok = ok && hipMemcpyAsync(s->seq_len, s->S.data(), batch * 4, hipMemcpyHostToDevice, st) == hipSuccess;
+  ok = ok && hipMemcpyAsync(s->rope, rope.data(), rope.size() * 4, hipMemcpyHostToDevice, st) == hipSuccess;
+  ok = ok && hipMemcpyAsync(s->err, &zero, 4, hipMemcpyHostToDevice, st) == hipSuccess;
+  // never-written cache rows read as NaN
+  ok = ok && hipMemsetAsync(s->kc, 0xff, kv_bytes, st) == hipSuccess;
+  ok = ok && hipMemsetAsync(s->vc, 0xff, kv_bytes, st) == hipSuccess;
+  ok = ok && hipStreamSynchronize(st) == hipSuccess;
+  if (!ok) {
+    if (s->h_buf) (void)hipHostFree(s->h_buf);
+    delete s;
+    return fail(WD_ERR_DEVICE, "initial state upload failed");
+  }
+  m->live_seqs++;
+  *out = s;
+  return WD_OK;
+}
+
+wd_status wd_slide_window(wd_seq* s) {
+  if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
+  if (s->mode == 2) return fail(WD_ERR_STATE, "sequence is driven by wd_full_step");
+  if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
+  s->mode = 1;
+  return do_slide(s);
+}
+
+wd_status wd_refresh_buffer(wd_seq* s) {
+  if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
+  if (s->mode == 2) return fail(WD_ERR_STATE, "sequence is driven by wd_full_step");
+  if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
+  if (s->cnt.j != 0 || s->refreshed)
+    return fail(WD_ERR_STATE, "no phase waiting for its refresh (call wd_slide_window first)");
+  s->mode = 1;
+  return do_refresh(s);
+}
+
+wd_status wd_step(wd_seq* s, wd_step_out* out) {
+  if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
+  if (s->mode == 2) return fail(WD_ERR_STATE, "sequence is driven by wd_full_step");
+  if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
+  s->mode = 1;
+  if (s->cnt.phase_due()) WD_TRY(do_slide(s));
+  const bool refresh = s->cnt.j == 0;
+  int rows;
+  if (refresh) {
+    if (!s->refreshed) WD_TRY(do_refresh(s));
+    rows = 0;
+    for (int b = 0; b < s->B; ++b) rows += s->ctx[b];
+  } else {
+    WD_TRY(do_normal(s));
+    rows = s->B * (s->cnt.n_active() + s->cnt.dp);
+  }
+  const int nA = s->cnt.n_active();
+  const int nsel = s->cnt.n_decode();
+  WD_TRY(decide(s, nA));
+  const int step = s->t;
+  s->cnt.take_step();
+  s->t++;
+  if (out) return fetch_out(s, out, step, refresh ? 1 : 0, rows, nsel);
+  return WD_OK;
+}
+
+wd_status wd_full_step(wd_seq* s, wd_step_out* out) {
+  if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
+  if (s->mode == 1) return fail(WD_ERR_STATE, "sequence is driven by the windowed calls");
+  if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
+  s->mode = 2;
+  Rows r;
+  for (int b = 0; b < s->B; ++b) s->ctx[b] = s->S[b];
+  r.g = base_geom(s);
+  for (int b = 0; b < s->B; ++b) {
+    r.g.row0[b] = s->off[b];
+    r.g.nrows[b] = s->S[b];
+  }
+  r.M = (int)s->T;
+  r.n_act = s->cnt.u;
+  WD_TRY(forward(s, 2, r));
+  const int nA = s->cnt.u;
+  const int nsel = std::min(s->cnt.k, nA);
+  WD_TRY(decide(s, nA));
+  const int step = s->t;
+  s->cnt.u -= nsel;
+  s->t++;
+  if (out) return fetch_out(s, out, step, 1, (int)s->T, nsel);
+  return WD_OK;
+}
+
+wd_status wd_get_state(const wd_seq* s, int32_t* tokens, uint8_t* decoded, int32_t* t) {
+  if (!s || !tokens) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  hipStream_t st = s->m->stream;
+  WD_HIP(hipStreamSynchronize(st));
+  WD_HIP(hipMemcpy(tokens, s->x, s->T * 4, hipMemcpyDeviceToHost));
+  if (decoded) WD_HIP(hipMemcpy(decoded, s->dec, s->T, hipMemcpyDeviceToHost));
+  if (t) *t = s->t;
+  return WD_OK;
+}
+
+wd_status wd_debug_logits(const wd_seq* s, float* logits, int32_t* positions, int32_t capacity,
+                          int32_t* n_rows) {
+  if (!s || !logits || !n_rows) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  const int n = s->B * s->last_nA;
+  *n_rows = n;
+  if (capacity < n) return fail(WD_ERR_OUT_OF_MEMORY, "capacity %d < %d rows", capacity, n);
+  WD_HIP(hipStreamSynchronize(s->m->stream));
+  WD_HIP(hipMemcpy(logits, s->logits, (size_t)n * s->m->cfg.vocab * 4, hipMemcpyDeviceToHost));
+  if (positions) WD_HIP(hipMemcpy(positions, s->act_pos, (size_t)n * 4, hipMemcpyDeviceToHost));
+  return WD_OK;
+}
+
+wd_status wd_debug_kv(const wd_seq* s, int32_t layer, int32_t b, float* k, float* v,
+                      int32_t capacity, int32_t* ctx_len) {
+  if (!s || !k || !v || !ctx_len) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  const wd_model_config& c = s->m->cfg;
+  if (layer < 0 || layer >= c.n_layers || b < 0 || b >= s->B)
+    return fail(WD_ERR_INVALID_ARG, "layer or sequence out of range");
+  const int ctx = s->ctx[b] > 0 ? s->ctx[b] : s->S[b];
+  *ctx_len = ctx;
+  if (capacity < ctx) return fail(WD_ERR_OUT_OF_MEMORY, "capacity %d < %d positions", capacity, ctx);
+  hipStream_t st = s->m->stream;
+  const long KVd = (long)c.n_kv_heads * c.head_dim;
+  const int d = c.head_dim;
+  std::vector<float> tmp((size_t)ctx * d);
+  for (int which = 0; which < 2; ++which) {
+    const char* base = (const char*)(which ? s->vc : s->kc) + (size_t)layer * KVd * s->T * s->m->esz;
+    float* dst = which ? v : k;
+    for (int g = 0; g < c.n_kv_heads; ++g) {
+      const size_t row0 = ((size_t)g * s->T + s->off[b]) * d;
+      if (c.dtype == WD_DTYPE_BF16)
+        WD_HIP(wd::widen_rows<uint16_t>((const uint16_t*)base + row0, d, s->dbg, ctx, d, st));
+      else
+        WD_HIP(wd::widen_rows<float>((const float*)base + row0, d, s->dbg, ctx, d, st));
+      WD_HIP(hipStreamSynchronize(st));
+      WD_HIP(hipMemcpy(tmp.data(), s->dbg, tmp.size() * 4, hipMemcpyDeviceToHost));
+      for (int p = 0; p < ctx; ++p)
+        memcpy(dst + ((size_t)p * c.n_kv_heads + g) * d, tmp.data() + (size_t)p * d, d * 4);
+    }
+  }
+  return WD_OK;
+}
+
+void wd_free_seq(wd_seq* s) {
+  if (!s) return;
+  (void)hipStreamSynchronize(s->m->stream);
+  if (s->h_buf) (void)hipHostFree(s->h_buf);
+  s->m->live_seqs--;
+  delete s;
+}
+
+int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, int32_t max_steps,
+                int32_t* is_refresh, int32_t* ctx_len, int32_t* n_active, int32_t* n_rows,
+                int32_t* n_decode) {
+  std::string why;
+  if (n_prompt < 0 || gen_len < 1 || !win_valid(win, &why)) {
+    fail(WD_ERR_INVALID_ARG, "%s", why.empty() ? "bad prompt or generation length" : why.c_str());
+    return -1;
+  }
+  Counts c;
+  c.E = win->n_active + win->n_buffer;
+  c.R = win->refresh_every;
+  c.k = win->unmask_per_step;
+  c.na = win->n_active;
+  c.u = gen_len;
+  const int S = n_prompt + gen_len;
+  int t = 0, ctx = 0;
+  while (c.u > 0) {
+    bool refresh = false;
+    if (c.phase_due()) {
+      c.start_phase();
+      ctx = c.ctx(S);
+    }
+    refresh = c.j == 0;
+    if (t < max_steps) {
+      if (is_refresh) is_refresh[t] = refresh ? 1 : 0;
+      if (ctx_len) ctx_len[t] = ctx;
+      if (n_active) n_active[t] = c.n_active();
+      if (n_rows) n_rows[t] = refresh ? ctx : c.n_active() + c.dp;
+      if (n_decode) n_decode[t] = c.n_decode();
+    }
+    c.take_step();
+    ++t;
+  }
+  return t;
+}
+
+}  // extern "C"

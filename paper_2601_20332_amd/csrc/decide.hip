@@ -1,0 +1,265 @@
+// Decisions of a step and the window bookkeeping, on the device.
+//
+// Per sequence b, positions p in [0, S_b) map to index off[b] + p of the
+// token / decoded-flag arrays.  decoded0 is the decoded-flag snapshot taken at
+// the phase start, so "decoded in this phase" = decoded && !decoded0.
+#include <climits>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace wd {
+
+// ---- confidence: argmax ([MASK] excluded, lowest id on ties) and its softmax probability ----
+__global__ __launch_bounds__(1024) void k_confidence(const float* __restrict__ logits, int V,
+                                                     int mask_id, int32_t* __restrict__ tok,
+                                                     float* __restrict__ conf) {
+  __shared__ float bv[16];
+  __shared__ int bi[16];
+  __shared__ float red[16];
+  const float* L = logits + (long)blockIdx.x * V;
+  float best = -INFINITY;
+  int idx = INT_MAX;
+  for (int v = threadIdx.x; v < V; v += blockDim.x) {
+    if (v == mask_id) continue;
+    const float x = L[v];
+    if (x > best) {  // increasing v: the first maximum is kept
+      best = x;
+      idx = v;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(idx, o, 64);
+    if (ob > best || (ob == best && oi < idx)) {
+      best = ob;
+      idx = oi;
+    }
+  }
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    bv[w] = best;
+    bi[w] = idx;
+  }
+  __syncthreads();
+  best = bv[0];
+  idx = bi[0];
+  for (int i = 1; i < nw; ++i)
+    if (bv[i] > best || (bv[i] == best && bi[i] < idx)) {
+      best = bv[i];
+      idx = bi[i];
+    }
+  float s = 0.f;
+  for (int v = threadIdx.x; v < V; v += blockDim.x)
+    if (v != mask_id) s += expf(L[v] - best);
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) {
+    tok[blockIdx.x] = idx;
+    conf[blockIdx.x] = 1.0f / s;
+  }
+}
+
+hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* tok, float* conf,
+                      hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_confidence, dim3(n), dim3(1024), 0, st, logits, V, mask_id, tok, conf);
+  return hipGetLastError();
+}
+
+// ---- block-wide exclusive prefix count of a flag (blockDim.x multiple of 64) ----------
+__device__ __forceinline__ int block_prefix(bool f, int* wtot, int& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const unsigned long long m = __ballot(f);
+  const int in_wave = __popcll(m & ((1ull << lane) - 1ull));
+  __syncthreads();
+  if (lane == 0) wtot[w] = __popcll(m);
+  __syncthreads();
+  int before = 0;
+  total = 0;
+  for (int i = 0; i < nw; ++i) {
+    if (i < w) before += wtot[i];
+    total += wtot[i];
+  }
+  return before + in_wave;
+}
+
+// ---- row set of a step ----------------------------------------------------------------------
+// One workgroup per sequence walks positions [0, c) in order, so rows come
+// out sorted by position.  Active positions are the first n_act undecoded
+// ones (the internal window); rows:
+//   mode 0 (refresh): every position of [0, c), row = row0 + p
+//   mode 1 (normal):  active positions and positions decoded in the phase
+//   mode 2 (full):    every position of [0, S), every undecoded one active
+// err bit 0: the row or active count differs from the host's schedule.
+__global__ __launch_bounds__(1024) void k_build_rows(int mode, const uint8_t* __restrict__ dec,
+                                                     const uint8_t* __restrict__ dec0, int n_act,
+                                                     WdStepGeom g, int32_t* __restrict__ row_tok,
+                                                     int32_t* __restrict__ row_pos,
+                                                     int32_t* __restrict__ row_seq,
+                                                     int32_t* __restrict__ row_out,
+                                                     int32_t* __restrict__ act_pos,
+                                                     int32_t* __restrict__ err) {
+  __shared__ int wtot[16];
+  const int b = blockIdx.x;
+  const int off = g.off[b], c = g.ctx[b], row0 = g.row0[b], nrows = g.nrows[b];
+  int carry_u = 0, carry_o = 0;
+  for (int base = 0; base < c; base += blockDim.x) {
+    const int p = base + threadIdx.x;
+    const bool valid = p < c;
+    const bool d = valid ? dec[off + p] != 0 : true;
+    const bool und = valid && !d;
+    int tot_u, tot_o;
+    const int rank_u = carry_u + block_prefix(und, wtot, tot_u);
+    const bool act = und && rank_u < n_act;
+    bool online;
+    if (mode == 1)
+      online = act || (valid && d && dec0[off + p] == 0);
+    else
+      online = valid;
+    const int rank_o = carry_o + block_prefix(online, wtot, tot_o);
+    const int ro = mode == 1 ? rank_o : p;
+    if (online && ro < nrows) {
+      const int r = row0 + ro;
+      row_tok[r] = off + p;
+      row_pos[r] = p;
+      row_seq[r] = b;
+      row_out[r] = act ? b * n_act + rank_u : -1;
+    }
+    if (act) act_pos[b * n_act + rank_u] = p;
+    carry_u += tot_u;
+    carry_o += tot_o;
+  }
+  // A count that disagrees with the host's schedule is reported through err;
+  // the slots it left unwritten get harmless values so later kernels stay in
+  // bounds (position 0 of the sequence, no active row).
+  const int wrote_o = mode == 1 ? carry_o : c;
+  for (int i = wrote_o + threadIdx.x; i < nrows; i += blockDim.x) {
+    row_tok[row0 + i] = off;
+    row_pos[row0 + i] = 0;
+    row_seq[row0 + i] = b;
+    row_out[row0 + i] = -1;
+  }
+  for (int i = carry_u + threadIdx.x; i < n_act; i += blockDim.x) act_pos[b * n_act + i] = -1;
+  if (threadIdx.x == 0) {
+    if (wrote_o != nrows || carry_u < n_act) atomicOr(err, 1);
+  }
+}
+
+hipError_t build_rows(int mode, const uint8_t* decoded, const uint8_t* decoded0, int n_act,
+                      const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos, int32_t* row_seq,
+                      int32_t* row_out, int32_t* act_pos, int32_t* err, hipStream_t st) {
+  hipLaunchKernelGGL(k_build_rows, dim3(g.batch), dim3(1024), 0, st, mode, decoded, decoded0,
+                     n_act, g, row_tok, row_pos, row_seq, row_out, act_pos, err);
+  return hipGetLastError();
+}
+
+// ---- phase start ------------------------------------------------------------------------------
+__global__ void k_snapshot(const uint8_t* __restrict__ dec, uint8_t* __restrict__ dec0, long n) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+    dec0[i] = dec[i];
+}
+
+// err bit 1: c is not (E-th undecoded position + 1), or S when fewer remain.
+__global__ __launch_bounds__(1024) void k_check_window(const uint8_t* __restrict__ dec, int E,
+                                                       WdStepGeom g,
+                                                       const int32_t* __restrict__ seq_len,
+                                                       int32_t* __restrict__ err) {
+  __shared__ int red[16];
+  const int b = blockIdx.x;
+  const int off = g.off[b], c = g.ctx[b], S = seq_len[b];
+  int below = 0, all = 0;
+  for (int p = threadIdx.x; p < S; p += blockDim.x) {
+    const int u = dec[off + p] == 0;
+    all += u;
+    if (p < c) below += u;
+  }
+  int t;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int o = 32; o > 0; o >>= 1) {
+    below += __shfl_xor(below, o, 64);
+    all += __shfl_xor(all, o, 64);
+  }
+  if (lane == 0) red[w] = below;
+  __syncthreads();
+  t = 0;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  below = t;
+  __syncthreads();
+  if (lane == 0) red[w] = all;
+  __syncthreads();
+  t = 0;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  all = t;
+  if (threadIdx.x == 0) {
+    bool ok;
+    if (all >= E)
+      ok = below == E && c >= 1 && c <= S && dec[off + c - 1] == 0;
+    else
+      ok = c == S;
+    if (!ok) atomicOr(err, 2);
+  }
+}
+
+hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, long total, int E, const WdStepGeom& g,
+                 const int32_t* seq_len, int32_t* err, hipStream_t st) {
+  const int blocks = (int)std::min<long>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_snapshot, dim3(blocks), dim3(256), 0, st, decoded, decoded0, total);
+  hipLaunchKernelGGL(k_check_window, dim3(g.batch), dim3(1024), 0, st, decoded, E, g, seq_len, err);
+  return hipGetLastError();
+}
+
+// ---- top-k decode -------------------------------------------------------------------------------
+// Candidate i of sequence b (index b * n_act + i) ranks by (conf desc,
+// position asc); the k best are decoded.
+__global__ __launch_bounds__(256) void k_select_update(const int32_t* __restrict__ act_pos,
+                                                       const int32_t* __restrict__ act_tok,
+                                                       const float* __restrict__ act_conf,
+                                                       int n_act, int k, WdStepGeom g,
+                                                       const int32_t* __restrict__ seq_len,
+                                                       int32_t* __restrict__ x,
+                                                       uint8_t* __restrict__ dec,
+                                                       int32_t* __restrict__ sel_pos,
+                                                       int32_t* __restrict__ sel_tok,
+                                                       float* __restrict__ sel_conf) {
+  const int b = blockIdx.x;
+  const long base = (long)b * n_act;
+  for (int i = threadIdx.x; i < k; i += blockDim.x) {
+    sel_pos[b * k + i] = -1;
+    sel_tok[b * k + i] = -1;
+    sel_conf[b * k + i] = 0.f;
+  }
+  __syncthreads();
+  const int S = seq_len[b];
+  for (int i = threadIdx.x; i < n_act; i += blockDim.x) {
+    const float ci = act_conf[base + i];
+    const int pi = act_pos[base + i];
+    if (pi < 0 || pi >= S) continue;  // a slot the bookkeeping flagged as missing
+    int rank = 0;
+    for (int j = 0; j < n_act; ++j) {
+      const float cj = act_conf[base + j];
+      const int pj = act_pos[base + j];
+      if (pj < 0 || pj >= S) continue;
+      rank += (cj > ci) || (cj == ci && pj < pi);
+    }
+    if (rank < k) {
+      const int t = act_tok[base + i];
+      sel_pos[b * k + rank] = pi;
+      sel_tok[b * k + rank] = t;
+      sel_conf[b * k + rank] = ci;
+      x[g.off[b] + pi] = t;
+      dec[g.off[b] + pi] = 1;
+    }
+  }
+}
+
+hipError_t select_update(const int32_t* act_pos, const int32_t* act_tok, const float* act_conf,
+                         int n_act, int k, const WdStepGeom& g, const int32_t* seq_len, int32_t* x,
+                         uint8_t* decoded, int32_t* sel_pos, int32_t* sel_tok, float* sel_conf,
+                         hipStream_t st) {
+  hipLaunchKernelGGL(k_select_update, dim3(g.batch), dim3(256), 0, st, act_pos, act_tok, act_conf,
+                     n_act, k, g, seq_len, x, decoded, sel_pos, sel_tok, sel_conf);
+  return hipGetLastError();
+}
+
+}  // namespace wd

@@ -1,0 +1,78 @@
+// Host-side launch wrappers of the libwd kernels.  Every wrapper enqueues
+// on the given stream and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace wd {
+
+// ---- GEMM (gemm.hip) -------------------------------------------------------------
+struct GemmPlan {
+  int splits = 1;        // K splits = number of partial outputs
+  int ks_per_split = 0;  // 32-wide K steps per split
+  int grid = 0;
+};
+GemmPlan plan_gemm_bf16(int M, int N, int K);
+hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st);
+hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
+                     const GemmPlan& p, hipStream_t st);
+hipError_t gemm_f32(const float* X, int ldx, const float* W, float* C, int M, int N, int K,
+                    hipStream_t st);
+
+// ---- row-wise layer pieces (layer.hip) -------------------------------------------------
+// h[r] = emb[x[row_tok[r]]]; a[r] = RMSNorm(h[r]) * gamma
+template <typename T>
+hipError_t embed_norm(const int32_t* x, const int32_t* row_tok, const T* emb, const T* gamma,
+                      float eps, float* h, T* a, int M, int H, hipStream_t st);
+// h[r] += sum_s C[s][r]; a[dst(r)] = RMSNorm(h[r]) * gamma, dst(r) = row_out ? row_out[r] : r
+// (rows with dst < 0 are not normalized)
+template <typename T>
+hipError_t residual_norm(float* h, const float* C, int S, int M, int H, const T* gamma, float eps,
+                         T* a, const int32_t* row_out, hipStream_t st);
+// q/k/v from the QKV partials: bias, RoPE on q and k, store q; k and v go to
+// the cache rows row_tok[r] of this layer.
+template <typename T>
+hipError_t qkv_epilogue(const float* C, int S, int M, const T* bias, const float* rope_cs,
+                        const int32_t* row_pos, const int32_t* row_tok, int n_heads, int n_kv,
+                        int head_dim, T* q, T* kcache, T* vcache, long cache_rows, hipStream_t st);
+// out[r][f] = silu(g) * u with g = sum_s C[s][r][f], u = sum_s C[s][r][F + f]
+template <typename T>
+hipError_t swiglu(const float* C, int S, int M, int F, T* out, hipStream_t st);
+// Non-causal attention of the step's rows over cache rows [0, c) of their
+// sequence (rows of sequence b are g.row0[b] .. g.row0[b] + g.nrows[b] - 1).
+hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint16_t* vcache,
+                          long cache_rows, uint16_t* o, const WdStepGeom& g, int n_heads, int n_kv,
+                          int head_dim, hipStream_t st);
+hipError_t attention_f32(const float* q, const float* kcache, const float* vcache, long cache_rows,
+                         float* o, const int32_t* row_seq, int M, const WdStepGeom& g, int n_heads,
+                         int n_kv, int head_dim, hipStream_t st);
+
+// ---- decisions and bookkeeping (decide.hip) -------------------------------------------
+hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* tok, float* conf,
+                      hipStream_t st);
+// Row set of a step.  mode 0 = refresh ([0, c) of each sequence), 1 = normal
+// (active + phase-decoded positions), 2 = full ([0, S) of each sequence,
+// every undecoded position active).  Active rows of sequence b get compact
+// indices b * n_act + rank.
+hipError_t build_rows(int mode, const uint8_t* decoded, const uint8_t* decoded0, int n_act,
+                      const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos, int32_t* row_seq,
+                      int32_t* row_out, int32_t* act_pos, int32_t* err, hipStream_t st);
+// Phase start: decoded0 = decoded; checks each sequence's c against the flags.
+hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, long total, int E, const WdStepGeom& g,
+                 const int32_t* seq_len, int32_t* err, hipStream_t st);
+// Top-k decode of each sequence among its n_act candidates; writes tokens,
+// decoded flags and the step's selection (b * k + rank).
+hipError_t select_update(const int32_t* act_pos, const int32_t* act_tok, const float* act_conf,
+                         int n_act, int k, const WdStepGeom& g, const int32_t* seq_len, int32_t* x,
+                         uint8_t* decoded, int32_t* sel_pos, int32_t* sel_tok, float* sel_conf,
+                         hipStream_t st);
+// Utility: widen n dtype elements (strided rows) to fp32.
+template <typename T>
+hipError_t widen_rows(const T* src, long src_stride, float* dst, int rows, int cols, hipStream_t st);
+
+}  // namespace wd

@@ -1,0 +1,409 @@
+// Row-wise pieces of a decoder layer and the windowed attention.
+//
+// Row set: every kernel works on the step's rows r = 0..M-1.  Row r is
+// position row_pos[r] of sequence row_seq[r]; its token and its K/V cache row
+// are at index row_tok[r] of the concatenated token / cache arrays.
+// K/V cache of one layer: [n_kv][cache_rows][head_dim], cache_rows = total
+// positions of the batch.
+#include "common.h"
+#include "kernels.h"
+
+namespace wd {
+
+// ---- embedding gather + first RMSNorm ------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ x,
+                                                    const int32_t* __restrict__ row_tok,
+                                                    const T* __restrict__ emb,
+                                                    const T* __restrict__ gamma, float eps,
+                                                    float* __restrict__ h, T* __restrict__ a, int H) {
+  __shared__ float red[16];
+  const long r = blockIdx.x;
+  const T* e = emb + (long)x[row_tok[r]] * H;
+  float* hr = h + r * H;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) {
+    const float v = Elem<T>::load(e + i);
+    hr[i] = v;
+    ss += v * v;
+  }
+  const float inv = 1.0f / sqrtf(block_sum(ss, red) / (float)H + eps);
+  for (int i = threadIdx.x; i < H; i += blockDim.x)
+    a[r * H + i] = Elem<T>::from_f(hr[i] * inv * Elem<T>::load(gamma + i));
+}
+
+template <typename T>
+hipError_t embed_norm(const int32_t* x, const int32_t* row_tok, const T* emb, const T* gamma,
+                      float eps, float* h, T* a, int M, int H, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_embed_norm<T>, dim3(M), dim3(256), 0, st, x, row_tok, emb, gamma, eps, h, a, H);
+  return hipGetLastError();
+}
+
+// ---- residual add of split-K partials + RMSNorm -----------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
+                                                       const float* __restrict__ C, int S, int M,
+                                                       int H, const T* __restrict__ gamma,
+                                                       float eps, T* __restrict__ a,
+                                                       const int32_t* __restrict__ row_out) {
+  __shared__ float red[16];
+  const long r = blockIdx.x;
+  float* hr = h + r * H;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) {
+    float acc = 0.f;
+    for (int s = 0; s < S; ++s) acc += C[((long)s * M + r) * H + i];
+    const float v = hr[i] + acc;
+    hr[i] = v;
+    ss += v * v;
+  }
+  const int dst = row_out ? row_out[r] : (int)r;
+  if (dst < 0) return;  // uniform over the block
+  const float inv = 1.0f / sqrtf(block_sum(ss, red) / (float)H + eps);
+  for (int i = threadIdx.x; i < H; i += blockDim.x)
+    a[(long)dst * H + i] = Elem<T>::from_f(hr[i] * inv * Elem<T>::load(gamma + i));
+}
+
+template <typename T>
+hipError_t residual_norm(float* h, const float* C, int S, int M, int H, const T* gamma, float eps,
+                         T* a, const int32_t* row_out, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_residual_norm<T>, dim3(M), dim3(256), 0, st, h, C, S, M, H, gamma, eps, a,
+                     row_out);
+  return hipGetLastError();
+}
+
+// ---- QKV epilogue: split-K sum, bias, RoPE, q store, K/V cache scatter ------------------
+// Block (r, slot): slot < n_heads is a query head, then n_kv key heads, then
+// n_kv value heads.  Thread i handles the rotation pair (i, i + d/2).
+template <typename T>
+__global__ void k_qkv_epilogue(const float* __restrict__ C, int S, int M, int N,
+                               const T* __restrict__ bias, const float* __restrict__ rope_cs,
+                               const int32_t* __restrict__ row_pos,
+                               const int32_t* __restrict__ row_tok, int nh, int nkv, int d,
+                               T* __restrict__ q, T* __restrict__ kc, T* __restrict__ vc,
+                               long cache_rows) {
+  const int r = blockIdx.x, hs = blockIdx.y, i = threadIdx.x, half = d >> 1;
+  const int col = hs * d + i;
+  float x0 = 0.f, x1 = 0.f;
+  for (int s = 0; s < S; ++s) {
+    const float* cr = C + ((long)s * M + r) * N;
+    x0 += cr[col];
+    x1 += cr[col + half];
+  }
+  if (bias) {
+    x0 += Elem<T>::load(bias + col);
+    x1 += Elem<T>::load(bias + col + half);
+  }
+  if (hs < nh + nkv) {
+    const float* cs = rope_cs + ((long)row_pos[r] * half + i) * 2;
+    const float c = cs[0], sn = cs[1];
+    const float y0 = x0 * c - x1 * sn;
+    const float y1 = x1 * c + x0 * sn;
+    x0 = y0;
+    x1 = y1;
+  }
+  T* dst;
+  if (hs < nh) {
+    dst = q + (long)r * nh * d + hs * d;
+  } else if (hs < nh + nkv) {
+    dst = kc + ((long)(hs - nh) * cache_rows + row_tok[r]) * d;
+  } else {
+    dst = vc + ((long)(hs - nh - nkv) * cache_rows + row_tok[r]) * d;
+  }
+  dst[i] = Elem<T>::from_f(x0);
+  dst[i + half] = Elem<T>::from_f(x1);
+}
+
+template <typename T>
+hipError_t qkv_epilogue(const float* C, int S, int M, const T* bias, const float* rope_cs,
+                        const int32_t* row_pos, const int32_t* row_tok, int n_heads, int n_kv,
+                        int head_dim, T* q, T* kcache, T* vcache, long cache_rows, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  const int N = (n_heads + 2 * n_kv) * head_dim;
+  hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(M, n_heads + 2 * n_kv), dim3(head_dim / 2), 0, st, C,
+                     S, M, N, bias, rope_cs, row_pos, row_tok, n_heads, n_kv, head_dim, q, kcache,
+                     vcache, cache_rows);
+  return hipGetLastError();
+}
+
+// ---- SwiGLU -----------------------------------------------------------------------------
+template <typename T>
+__global__ void k_swiglu(const float* __restrict__ C, int S, int M, int F, T* __restrict__ out) {
+  const long total = (long)M * F;
+  for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (long)gridDim.x * blockDim.x) {
+    const long r = e / F;
+    const int f = (int)(e - r * F);
+    float g = 0.f, u = 0.f;
+    for (int s = 0; s < S; ++s) {
+      const float* cr = C + ((long)s * M + r) * (2L * F);
+      g += cr[f];
+      u += cr[F + f];
+    }
+    out[e] = Elem<T>::from_f(g / (1.0f + expf(-g)) * u);
+  }
+}
+
+template <typename T>
+hipError_t swiglu(const float* C, int S, int M, int F, T* out, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  const long total = (long)M * F;
+  const int blocks = (int)std::min<long>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(k_swiglu<T>, dim3(blocks), dim3(256), 0, st, C, S, M, F, out);
+  return hipGetLastError();
+}
+
+// ---- attention, fp32 models: one wave per (row, head) ------------------------------------
+// Scores for keys lane, lane + 64, ... are kept in LDS (dynamic, ctx floats).
+__global__ __launch_bounds__(64) void k_attn_f32(const float* __restrict__ q,
+                                                 const float* __restrict__ kc,
+                                                 const float* __restrict__ vc, long cache_rows,
+                                                 float* __restrict__ o,
+                                                 const int32_t* __restrict__ row_seq,
+                                                 WdStepGeom g, int nh, int nkv, int d) {
+  extern __shared__ float p[];
+  __shared__ float qs[128];
+  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int b = row_seq[r];
+  const int c = g.ctx[b];
+  const long off = g.off[b];
+  const int kvh = h / (nh / nkv);
+  const float* kb = kc + ((long)kvh * cache_rows + off) * d;
+  const float* vb = vc + ((long)kvh * cache_rows + off) * d;
+  for (int i = lane; i < d; i += 64) qs[i] = q[(long)r * nh * d + h * d + i];
+  __syncthreads();
+  const float scale = 1.0f / sqrtf((float)d);
+  float mx = -INFINITY;
+  for (int j = lane; j < c; j += 64) {
+    const float* kr = kb + (long)j * d;
+    float s = 0.f;
+    for (int i = 0; i < d; ++i) s = fmaf(qs[i], kr[i], s);
+    s *= scale;
+    p[j] = s;
+    mx = fmaxf(mx, s);
+  }
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int j = lane; j < c; j += 64) {
+    const float e = expf(p[j] - mx);
+    p[j] = e;
+    sum += e;
+  }
+  sum = wave_sum(sum);
+  __syncthreads();
+  for (int i = lane; i < d; i += 64) {
+    float acc = 0.f;
+    for (int j = 0; j < c; ++j) acc = fmaf(p[j], vb[(long)j * d + i], acc);
+    o[(long)r * nh * d + h * d + i] = acc / sum;
+  }
+}
+
+// ---- attention, bf16 models: flash-style with MFMA (head_dim 128) ----------------------------
+// Workgroup = (query head, sequence, block of 64 query rows); wave w owns 16
+// query rows.  Keys go in tiles of 64 through LDS: K row-major (A operand of
+// S^T = K Q^T) and V transposed (A operand of O^T = V^T P^T), so the scores
+// stay in registers in exactly the layout the second product needs.  Softmax
+// runs online in fp32; P enters the bf16 MFMA as hi + lo bf16 parts, which
+// keeps P V at fp32-level accuracy.
+constexpr int kAttD = 128;
+constexpr int kKT = 64;              // keys per tile
+constexpr int kKPitch = kAttD + 8;   // bf16 elements per K row in LDS
+constexpr int kVPitch = kKT + 8;     // bf16 elements per V^T row in LDS
+
+__global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ q,
+                                                   const uint16_t* __restrict__ kc,
+                                                   const uint16_t* __restrict__ vc,
+                                                   long cache_rows, uint16_t* __restrict__ o,
+                                                   WdStepGeom g, int nh, int nkv) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKT * kKPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[kAttD * kVPitch];
+  const int h = blockIdx.x, b = blockIdx.y, qb = blockIdx.z;
+  const int nq = g.nrows[b];
+  if (qb * 64 >= nq) return;
+  const int c = g.ctx[b];
+  const long off = g.off[b];
+  const int row0 = g.row0[b];
+  const int kvh = h / (nh / nkv);
+  const uint16_t* kb = kc + ((long)kvh * cache_rows + off) * kAttD;
+  const uint16_t* vb = vc + ((long)kvh * cache_rows + off) * kAttD;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int qi = qb * 64 + wave * 16 + l16;  // this lane's query (column of S^T / O^T)
+  const bool qvalid = qi < nq;
+  const bool wave_active = qb * 64 + wave * 16 < nq;
+  const long ldq = (long)nh * kAttD;
+
+  u32x4 qf[4];
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int cc = 0; cc < 4; ++cc)
+    qf[cc] = qvalid ? *(const u32x4*)(q + (long)(row0 + qi) * ldq + h * kAttD + cc * 32 + grp * 8)
+                    : zero4;
+
+  f32x4 oacc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) oacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float scale = 0.08838834764831845f;  // 1/sqrt(128)
+
+  for (int j0 = 0; j0 < c; j0 += kKT) {
+    __syncthreads();
+    // K tile: 64 rows x 256 B; V tile transposed into Vt[dd][key]
+    for (int e = tid; e < kKT * 16; e += 256) {
+      const int key = e >> 4, ch = e & 15;
+      u32x4 kv = zero4, vv = zero4;
+      if (j0 + key < c) {
+        kv = *(const u32x4*)(kb + (long)(j0 + key) * kAttD + ch * 8);
+        vv = *(const u32x4*)(vb + (long)(j0 + key) * kAttD + ch * 8);
+      }
+      *(u32x4*)(Ks + key * kKPitch + ch * 8) = kv;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        Vt[(ch * 8 + 2 * i) * kVPitch + key] = (uint16_t)(vv[i] & 0xffffu);
+        Vt[(ch * 8 + 2 * i + 1) * kVPitch + key] = (uint16_t)(vv[i] >> 16);
+      }
+    }
+    __syncthreads();
+    if (!wave_active) continue;
+
+    // S^T[key][query] for 4 subtiles of 16 keys
+    f32x4 sacc[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      sacc[st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const u32x4 ka = *(const u32x4*)(Ks + (st * 16 + l16) * kKPitch + cc * 32 + grp * 8);
+        sacc[st] = mfma16(ka, qf[cc], sacc[st]);
+      }
+    }
+    // this lane holds keys st*16 + grp*4 + jj for query l16
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int key = j0 + st * 16 + grp * 4 + jj;
+        const float s = key < c ? sacc[st][jj] * scale : -INFINITY;
+        sacc[st][jj] = s;
+        tmax = fmaxf(tmax, s);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float m_new = fmaxf(m_run, tmax);
+    const float corr = expf(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const float pv = expf(sacc[st][jj] - m_new);
+        sacc[st][jj] = pv;
+        psum += pv;
+      }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * corr + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) oacc[i] *= corr;
+
+    // O^T += V^T P^T over two 32-key chunks (subtiles 2pc, 2pc+1)
+#pragma unroll
+    for (int pc = 0; pc < 2; ++pc) {
+      // element e of the fragment is key index (e < 4 ? subtile 2pc : 2pc+1), row grp*4 + e%4
+      u32x4 bhi, blo;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4& sp = sacc[2 * pc + (i >> 1)];
+        const float p0 = sp[(2 * i) & 3], p1 = sp[(2 * i + 1) & 3];
+        const uint16_t h0 = f2bf(p0), h1 = f2bf(p1);
+        bhi[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        blo[i] = (uint32_t)f2bf(p0 - bf2f(h0)) | ((uint32_t)f2bf(p1 - bf2f(h1)) << 16);
+      }
+#pragma unroll
+      for (int df = 0; df < 8; ++df) {
+        const uint16_t* vrow = Vt + (df * 16 + l16) * kVPitch;
+        const u32x2 v0 = *(const u32x2*)(vrow + (2 * pc) * 16 + grp * 4);
+        const u32x2 v1 = *(const u32x2*)(vrow + (2 * pc + 1) * 16 + grp * 4);
+        const u32x4 va = {v0.x, v0.y, v1.x, v1.y};
+        oacc[df] = mfma16(va, bhi, oacc[df]);
+        oacc[df] = mfma16(va, blo, oacc[df]);
+      }
+    }
+  }
+  if (!qvalid) return;
+  const float inv = 1.0f / l_run;
+  uint16_t* orow = o + (long)(row0 + qi) * ldq + h * kAttD;
+#pragma unroll
+  for (int df = 0; df < 8; ++df) {
+    u32x2 w;
+    w.x = (uint32_t)f2bf(oacc[df][0] * inv) | ((uint32_t)f2bf(oacc[df][1] * inv) << 16);
+    w.y = (uint32_t)f2bf(oacc[df][2] * inv) | ((uint32_t)f2bf(oacc[df][3] * inv) << 16);
+    *(u32x2*)(orow + df * 16 + grp * 4) = w;
+  }
+}
+
+hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint16_t* vcache,
+                          long cache_rows, uint16_t* o, const WdStepGeom& g, int n_heads, int n_kv,
+                          int head_dim, hipStream_t st) {
+  if (head_dim != kAttD) return hipErrorInvalidValue;
+  int nqmax = 0;
+  for (int b = 0; b < g.batch; ++b) nqmax = std::max(nqmax, g.nrows[b]);
+  if (nqmax <= 0) return hipSuccess;
+  dim3 grid(n_heads, g.batch, (nqmax + 63) / 64);
+  hipLaunchKernelGGL(k_attn_bf16, grid, dim3(256), 0, st, q, kcache, vcache, cache_rows, o, g,
+                     n_heads, n_kv);
+  return hipGetLastError();
+}
+
+hipError_t attention_f32(const float* q, const float* kcache, const float* vcache, long cache_rows,
+                         float* o, const int32_t* row_seq, int M, const WdStepGeom& g, int n_heads,
+                         int n_kv, int head_dim, hipStream_t st) {
+  int cmax = 0;
+  for (int b = 0; b < g.batch; ++b) cmax = std::max(cmax, g.ctx[b]);
+  if (M <= 0) return hipSuccess;
+  if (head_dim > 128 || cmax > 16384) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_attn_f32, dim3(M, n_heads), dim3(64), cmax * sizeof(float), st, q, kcache,
+                     vcache, cache_rows, o, row_seq, g, n_heads, n_kv, head_dim);
+  return hipGetLastError();
+}
+
+// ---- fp32 copies for debugging --------------------------------------------------------------
+template <typename T>
+__global__ void k_widen(const T* __restrict__ src, long stride, float* __restrict__ dst, int rows,
+                        int cols) {
+  const long total = (long)rows * cols;
+  for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (long)gridDim.x * blockDim.x) {
+    const long r = e / cols;
+    dst[e] = Elem<T>::to_f(src[r * stride + (e - r * cols)]);
+  }
+}
+
+template <typename T>
+hipError_t widen_rows(const T* src, long src_stride, float* dst, int rows, int cols,
+                      hipStream_t st) {
+  const long total = (long)rows * cols;
+  if (total <= 0) return hipSuccess;
+  const int blocks = (int)std::min<long>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_widen<T>, dim3(blocks), dim3(256), 0, st, src, src_stride, dst, rows, cols);
+  return hipGetLastError();
+}
+
+#define WD_INSTANTIATE(T)                                                                       \
+  template hipError_t embed_norm<T>(const int32_t*, const int32_t*, const T*, const T*, float,   \
+                                    float*, T*, int, int, hipStream_t);                          \
+  template hipError_t residual_norm<T>(float*, const float*, int, int, int, const T*, float, T*, \
+                                       const int32_t*, hipStream_t);                             \
+  template hipError_t qkv_epilogue<T>(const float*, int, int, const T*, const float*,            \
+                                      const int32_t*, const int32_t*, int, int, int, T*, T*, T*, \
+                                      long, hipStream_t);                                        \
+  template hipError_t swiglu<T>(const float*, int, int, int, T*, hipStream_t);                   \
+  template hipError_t widen_rows<T>(const T*, long, float*, int, int, hipStream_t);
+WD_INSTANTIATE(float)
+WD_INSTANTIATE(uint16_t)
+
+}  // namespace wd

@@ -1,0 +1,162 @@
+"""Shared helpers of the GPU parity tests: run a generation through the C ABI,
+replay it in the oracle, compare step by step.
+
+Logits of the active rows, per row max|gpu - oracle| / max|oracle|: at most
+1e-4 for fp32 models and 2e-2 for bf16 models.
+
+Decoded positions must be identical, except where the logit errors already
+measured make the oracle's ranking uncertain: a sup-norm logit error d moves
+log(conf) = l_top - logsumexp(l) by at most 2d, so two candidates i, j can
+rank differently only if |log c_i - log c_j| <= 2 (d_i + d_j).  Inside that
+band the oracle adopts the GPU's choice, which must itself be the top-k of
+the GPU's own logits.  fp32 models must match with no adoption.  A decoded
+token must equal the oracle's wherever the oracle's top-1 logit margin
+exceeds 1e-2, and is adopted otherwise.  Adoptions are counted; callers bound
+them.
+"""
+from __future__ import annotations
+
+import dataclasses
+import sys
+from typing import Dict, List, Optional
+
+import numpy as np
+
+import synth
+from oracle.model import OracleModel
+from oracle.sampler import top1_margin
+from oracle.schedule import FullDecoder, WindowedDecoder
+
+LOGIT_TOL = {synth.DTYPE_F32: 1e-4, synth.DTYPE_BF16: 2e-2}
+MARGIN = 1e-2
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def cfg_of(shape: synth.ModelShape):
+    import paper_2601_20332_amd as wd
+    return wd.model_config(n_layers=shape.n_layers, hidden=shape.hidden, n_heads=shape.n_heads,
+                           n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn=shape.ffn,
+                           vocab=shape.vocab, mask_id=shape.mask_id, dtype=shape.dtype,
+                           qkv_bias=shape.qkv_bias, rms_eps=shape.rms_eps,
+                           rope_theta=shape.rope_theta)
+
+
+def gpu_model(W: synth.Weights, device="cuda"):
+    """Uploads the seeded weights and packs them (the originals are dropped)."""
+    import torch
+    import paper_2601_20332_amd as wd
+    ts = []
+    for _, raw in W.iter_raw(workers=8):
+        a = raw.view(np.int16) if raw.dtype == np.uint16 else raw
+        ts.append(torch.from_numpy(np.ascontiguousarray(a)).to(device))
+    m = wd.wd_init_model(cfg_of(W.shape), ts, device)
+    del ts
+    return m
+
+
+@dataclasses.dataclass
+class GpuStep:
+    res: object                   # StepResult
+    logits: np.ndarray            # active-row logits [n, V]
+    positions: np.ndarray         # their positions (sequence after sequence)
+
+
+def run_gpu(model, prompts, gen_len, win: synth.WindowSettings, full: bool = False,
+            max_steps: Optional[int] = None, keep_logits: bool = True) -> List[GpuStep]:
+    import paper_2601_20332_amd as wd
+    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
+    gen = wd.wd_prefill_prompt(model, prompts, gen_len, wc)
+    steps = []
+    try:
+        n = 0
+        while max_steps is None or n < max_steps:
+            try:
+                r = (wd.wd_full_step if full else wd.wd_step)(gen)
+            except wd.WdError as e:
+                if e.status == wd.WD_ERR_STATE:
+                    break
+                raise
+            lg, pos = wd.wd_debug_logits(gen) if keep_logits else (None, None)
+            steps.append(GpuStep(r, lg, pos))
+            n += 1
+        final = wd.wd_get_state(gen)
+    finally:
+        gen.free()
+    return steps, final
+
+
+@dataclasses.dataclass
+class Report:
+    steps: int = 0
+    max_rel: float = 0.0
+    token_adopted: int = 0
+    select_adopted: int = 0
+
+
+def rel_err(g: np.ndarray, o: np.ndarray) -> np.ndarray:
+    return np.abs(g - o).max(axis=1) / np.abs(o).max(axis=1)
+
+
+def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuStep], b: int,
+                   batch: int, full: bool = False, max_steps: Optional[int] = None) -> Report:
+    """Replays sequence b of a GPU generation in the oracle and compares every step."""
+    dtype = om.shape.dtype
+    tol = LOGIT_TOL[dtype]
+    rep = Report()
+    dec = (FullDecoder(om, prompt, gen_len, win.unmask_per_step) if full
+           else WindowedDecoder(om, prompt, gen_len, win))
+    for t, gs in enumerate(gpu_steps):
+        if max_steps is not None and t >= max_steps:
+            break
+        k = win.unmask_per_step
+        n_act_rows = len(gs.positions) // batch
+        g_pos = gs.positions[b * n_act_rows:(b + 1) * n_act_rows]
+        g_log = gs.logits[b * n_act_rows:(b + 1) * n_act_rows]
+        g_sel = [int(p) for p in gs.res.positions[b] if p >= 0]
+        g_tok = {int(p): int(tk) for p, tk in zip(gs.res.positions[b], gs.res.tokens[b]) if p >= 0}
+
+        def override(rec):
+            assert rec.active == g_pos.tolist(), (t, rec.active, g_pos.tolist())
+            err = rel_err(g_log, rec.logits)
+            rep.max_rel = max(rep.max_rel, float(err.max()))
+            assert err.max() <= tol, f"step {t}: logits max rel err {err.max():.3e} > {tol}"
+            sel = list(rec.selected)
+            if sorted(sel) != sorted(g_sel):
+                assert dtype != synth.DTYPE_F32, f"step {t}: selected {g_sel} vs oracle {sel}"
+                d = np.abs(g_log - rec.logits).max(axis=1)
+                lc = np.log(rec.conf.astype(np.float64))
+                idx = {p: i for i, p in enumerate(rec.active)}
+                for pi in set(g_sel) - set(sel):
+                    for pj in set(sel) - set(g_sel):
+                        i, j = idx[pi], idx[pj]
+                        assert lc[j] - lc[i] <= 2 * (d[i] + d[j]) + 1e-6, (
+                            f"step {t}: GPU chose {pi} over {pj}: log-conf gap "
+                            f"{lc[j] - lc[i]:.3e} > 2(d_i + d_j) = {2 * (d[i] + d[j]):.3e}")
+                # the GPU's choice is the top-k of its own logits
+                from oracle.sampler import confidence as _conf
+                _, gc = _conf(g_log, om.shape.mask_id)
+                gl = np.log(gc.astype(np.float64))
+                worst_in = min(gl[idx[p]] for p in g_sel)
+                best_out = max([gl[i] for p, i in idx.items() if p not in g_sel], default=-np.inf)
+                assert worst_in >= best_out - 1e-6, f"step {t}: GPU selection not its own top-k"
+                rep.select_adopted += 1
+                sel = g_sel
+            toks = {}
+            margins = top1_margin(rec.logits, om.shape.mask_id)
+            for p in sel:
+                i = rec.active.index(p)
+                ot = int(rec.tokens[i])
+                if ot != g_tok[p]:
+                    assert margins[i] <= MARGIN, (
+                        f"step {t} pos {p}: token {g_tok[p]} vs oracle {ot}, margin {margins[i]:.3e}")
+                    rep.token_adopted += 1
+                toks[p] = g_tok[p]
+            return sel, toks
+
+        dec.step(override=override, keep_logits=True)
+        rep.steps += 1
+    return rep
