@@ -1,0 +1,278 @@
+#!/usr/bin/env python3
+"""Throughput of Window-Diffusion decoding on one MI355X.
+
+Workload (default): the LLaDA-8B shape in bf16 (32 layers, hidden 4096,
+32 heads x 128, SwiGLU 12288, vocabulary 126464) with seeded random-init
+weights N(0, 0.02); batch 1, a 128-token random prompt and 256 masked
+positions; 32 active + 64 buffer positions, refresh every 8 steps, 1 token
+unmasked per step.
+
+One bench step is one whole generation: wd_prefill_prompt plus every
+denoising step (refresh and normal steps) until all 256 positions are
+decoded.  `value` is denoising steps per second over the timed generations.
+Also reported: decoded tokens/s, the speedup over standard full-sequence
+decoding on the same GPU and kernels, the roofline of the dominant kernel
+(the projection GEMM, timed with HIP events on the library's stream) and the
+CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "denoising steps/s + decoded tokens/s at LLaDA-8B shape, 1 GPU; MFMA/HBM % peak"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_traffic.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2601_20332_amd", "csrc", "gemm.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def gemm_source_hash() -> str:
+    return hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per GEMM launch from the committed rocprofv3 counter runs, if they
+    were taken on the current kernel source."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("gemm_source_sha256_16") != gemm_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def upload_model(shape, device):
+    import numpy as np
+    import torch
+    import synth
+    import paper_2601_20332_amd as wd
+    W = synth.Weights(shape)
+    ts = []
+    for _, raw in W.iter_raw(workers=min(16, os.cpu_count() or 4)):
+        a = raw.view(np.int16) if raw.dtype == np.uint16 else raw
+        ts.append(torch.from_numpy(np.ascontiguousarray(a)).to(device))
+    cfg = wd.model_config(n_layers=shape.n_layers, hidden=shape.hidden, n_heads=shape.n_heads,
+                          n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn=shape.ffn,
+                          vocab=shape.vocab, mask_id=shape.mask_id, dtype=shape.dtype,
+                          qkv_bias=shape.qkv_bias, rms_eps=shape.rms_eps,
+                          rope_theta=shape.rope_theta)
+    m = wd.wd_init_model(cfg, ts, device)
+    del ts
+    torch.cuda.empty_cache()
+    return m
+
+
+def generation(model, prompts, G, wc, n_steps, full=False):
+    import paper_2601_20332_amd as wd
+    gen = wd.wd_prefill_prompt(model, prompts, G, wc)
+    fn = wd.lib.wd_full_step if full else wd.lib.wd_step
+    for _ in range(n_steps):
+        wd._check(fn(gen.handle, None))
+    gen.free()  # synchronizes the stream
+
+
+def cpu_baseline(w, plan):
+    """The float64 oracle on a bounded sample of the workload: one refresh forward
+    (the largest retained prefix of the generation) and one normal-step forward
+    (the average online row count), both over 2 of the layers, plus the LM head
+    and confidence on the active rows.  Scaled to the full depth and summed over
+    the generation's schedule (cost per layer taken as linear in the rows)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    import synth
+    from oracle.model import OracleModel
+    from oracle.sampler import confidence
+    L_s = 2
+    shape = synth.with_layers(w.model, L_s)
+    om = OracleModel(synth.Weights(shape), cache_budget_bytes=64e9)
+    for name, _, _ in synth.tensor_specs(shape):
+        if name != "emb":
+            om.w(name)                                    # weights resident before timing
+    S = w.prompt_len + w.gen_len
+    prompt = synth.prompts(shape, [w.prompt_len])[0]
+    x = np.concatenate([prompt, np.full(w.gen_len, shape.mask_id)])
+    c_ref = max(p.ctx_len for p in plan if p.refresh)
+    normal = [p.n_online for p in plan if not p.refresh]
+    m_norm = int(round(sum(normal) / max(1, len(normal))))
+    n_act = w.window.n_active
+    t0 = time.perf_counter()
+    h, K, V = om.forward(x[:c_ref])
+    t1 = time.perf_counter()
+    cache = om.new_cache(S)
+    for l in range(L_s):
+        cache.K[l][:c_ref] = K[l]
+        cache.V[l][:c_ref] = V[l]
+    rows = list(range(w.prompt_len, w.prompt_len + m_norm))
+    t2 = time.perf_counter()
+    om.forward_rows(x[rows], rows, cache, c_ref)
+    t3 = time.perf_counter()
+    confidence(om.logits(h[:n_act]), shape.mask_id)
+    t4 = time.perf_counter()
+    per_row_ref = (t1 - t0) / L_s / c_ref
+    per_row_norm = (t3 - t2) / L_s / m_norm
+    head = t4 - t3
+    L = w.model.n_layers
+    total = sum(L * (per_row_ref * p.n_online if p.refresh else per_row_norm * p.n_online) + head
+                for p in plan)
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {
+        "value": len(plan) / total,
+        "unit": "steps/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"float64 oracle, {L_s} of {L} layers: refresh forward over {c_ref} rows "
+                   f"({t1 - t0:.1f} s), normal-step forward over {m_norm} rows ({t3 - t2:.1f} s), "
+                   f"LM head + confidence on {n_act} rows ({head:.1f} s); scaled to {L} layers "
+                   f"and the {len(plan)}-step schedule (extrapolated)"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3, help="timed whole generations")
+    ap.add_argument("--warmup", type=int, default=1, help="untimed whole generations")
+    ap.add_argument("--workload", default="llada8b",
+                    choices=["llada8b", "dream7b", "llada8b_long"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-full", action="store_true", help="skip the full-sequence comparison")
+    ap.add_argument("--no-events", action="store_true",
+                    help="time without the per-launch GEMM events (no roofline)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the windowed step of one batch runs on one MI355X "
+              "(no multi-GPU path is built); run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2601_20332_amd as wd
+
+    w = synth.WORKLOADS[args.workload]
+    device = "cuda:0"
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    model = upload_model(w.model, device)
+    log(f"[bench] {args.workload}: weights generated and packed in {time.time() - t0:.1f}s")
+    prompts = synth.prompts(w.model, synth.prompt_lengths(w))
+    win = w.window
+    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
+    n_steps = len(wd.wd_plan(w.prompt_len, w.gen_len, wc)["n_rows"])
+
+    for i in range(args.warmup):
+        generation(model, prompts, w.gen_len, wc, n_steps)
+        log(f"[bench] warmup generation {i + 1}/{args.warmup} done")
+
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        generation(model, prompts, w.gen_len, wc, n_steps)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    log(f"[bench] {args.steps} timed generations in {elapsed:.3f}s")
+
+    # Roofline of the dominant kernel: the same generations again, now with a
+    # HIP event pair around every projection-GEMM launch on the library's stream
+    # (kept out of the pass above, whose clock gives `value`).
+    roofline = None
+    if not args.no_events:
+        wd.wd_profile_enable(model, True)
+        torch.cuda.synchronize()
+        t_ev = time.perf_counter()
+        for i in range(args.steps):
+            generation(model, prompts, w.gen_len, wc, n_steps)
+        torch.cuda.synchronize()
+        elapsed_ev = time.perf_counter() - t_ev
+        launches, ms, alg_bytes, alg_flops = wd.wd_profile_read(model)
+        wd.wd_profile_enable(model, False)
+        if launches > 0 and ms > 0:
+            avg_s = ms / 1e3 / launches
+            achieved = alg_bytes / launches / avg_s / 1e9
+            roofline = {
+                "kernel": "k_gemm_bf16 (all projection and LM-head GEMM launches)",
+                "bound": "hbm",
+                "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS,
+                "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(),
+                "launches": launches,
+                "avg_launch_us": round(avg_s * 1e6, 2),
+                "alg_bytes_per_launch": round(alg_bytes / launches),
+                "mfma_tflops": round(alg_flops / (ms / 1e3) / 1e12, 1),
+                "mfma_frac": round(alg_flops / (ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                "share_of_step_time": round(ms / 1e3 / elapsed_ev, 3),
+                "instrumented_pass_s": round(elapsed_ev, 3),
+            }
+
+    full_speedup = None
+    if not args.no_full:
+        generation(model, prompts, w.gen_len, wc, n_steps, full=True)  # warm
+        torch.cuda.synchronize()
+        tf = time.perf_counter()
+        generation(model, prompts, w.gen_len, wc, n_steps, full=True)
+        torch.cuda.synchronize()
+        t_full = time.perf_counter() - tf
+        full_speedup = round(t_full / (elapsed / args.steps), 3)
+        log(f"[bench] full-sequence generation {t_full:.3f}s")
+    model.free()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle.schedule import plan_counts
+        plan = plan_counts(w.prompt_len, w.gen_len, win)
+        cpu = cpu_baseline(w, plan)
+        log(f"[bench] cpu baseline: {cpu}")
+
+    B = len(prompts)
+    steps_per_s = args.steps * n_steps / elapsed
+    out = {
+        "metric": METRIC,
+        "value": round(steps_per_s, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{args.workload}: {w.model.n_layers}L hidden {w.model.hidden} "
+                         f"{w.model.n_heads}q/{w.model.n_kv_heads}kv x {w.model.head_dim} "
+                         f"ffn {w.model.ffn} vocab {w.model.vocab}, random init N(0,0.02)"),
+            "batch": B,
+            "prompt_len": w.prompt_len,
+            "gen_len": w.gen_len,
+            "n_active": win.n_active,
+            "n_buffer": win.n_buffer,
+            "refresh_every": win.refresh_every,
+            "unmask_per_step": win.unmask_per_step,
+            "bench_step": f"one whole generation = {n_steps} denoising steps",
+        },
+        "decoded_tokens_per_s": round(args.steps * B * w.gen_len / elapsed, 3),
+        "speedup_vs_full_sequence": full_speedup,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

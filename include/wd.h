@@ -139,13 +139,14 @@ size_t wd_seq_bytes(const wd_model* m, const wd_window_config* win, int32_t batc
 /* Starts a generation (Sec. 3.1 initial state): sequence b is its prompt
  * (prompt_lens[b] ids taken in order from the concatenated host array
  * prompt_ids) followed by gen_len [MASK] tokens; prompt positions count as
- * decoded.  Then runs the first phase's slide and refresh (wd_slide_window,
- * wd_refresh_buffer), so the next wd_step is step 0, the phase's refresh
- * step.  `workspace` is caller-owned device memory of >= wd_seq_bytes bytes.
+ * decoded and t = 0.  Uploads the state and the RoPE table; the first step
+ * (wd_step or wd_full_step) starts the first phase.  `workspace` is
+ * caller-owned device memory of >= wd_seq_bytes bytes; never-written K/V
+ * cache rows are filled with NaN.  Synchronizes the stream.
  * Errors: WD_ERR_INVALID_ARG (ids outside [0, vocab), NULL pointers,
- * batch < 1, gen_len < 1, n_active < 1, n_buffer < 0, refresh_every < 1,
- * unmask_per_step < 1), WD_ERR_OUT_OF_MEMORY (workspace too small),
- * WD_ERR_DEVICE. */
+ * batch outside [1, 64], gen_len < 1, n_active outside [1, 64], n_buffer < 0,
+ * refresh_every < 1, unmask_per_step < 1), WD_ERR_OUT_OF_MEMORY (workspace
+ * too small), WD_ERR_DEVICE. */
 wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_t* prompt_lens,
                             int32_t batch, int32_t gen_len, const wd_window_config* win,
                             void* workspace, size_t ws_bytes, wd_seq** out);
@@ -207,6 +208,24 @@ wd_status wd_debug_kv(const wd_seq* s, int32_t layer, int32_t b, float* k, float
                       int32_t capacity, int32_t* ctx_len);
 
 void wd_free_seq(wd_seq* s); /* NULL is a no-op; synchronizes the stream */
+
+/* ---- kernel timing ------------------------------------------------------------- */
+
+/* When enabled, every launch of the projection GEMM kernel (Q/K/V, output,
+ * gate/up, down and LM-head products) on this model's stream is bracketed by
+ * a pair of HIP events, and the launch's algorithmic traffic and work are
+ * recorded: bytes = weights (N*K elements) + input rows (M*K elements) +
+ * fp32 output (M*N*4), flops = 2*M*N*K.  Up to 1 << 20 launches are kept
+ * between reads (WD_ERR_OUT_OF_MEMORY from the launching call beyond that).
+ * Disabled by default; enabling or disabling discards unread records. */
+wd_status wd_profile_enable(wd_model* m, int32_t enable);
+
+/* Synchronizes the model's stream, then returns the launches recorded since
+ * the last read, the sum of their event-measured durations (milliseconds) and
+ * of their algorithmic bytes and flops, and clears the records.  Any output
+ * pointer may be NULL. */
+wd_status wd_profile_read(wd_model* m, int64_t* launches, double* total_ms, double* alg_bytes,
+                          double* alg_flops);
 
 /* ---- host-only helpers -------------------------------------------------------- */
 

@@ -29,7 +29,8 @@ WD_DTYPE_BF16 = 1
 EXPORTED = ["wd_weight_count", "wd_weight_shape", "wd_model_bytes", "wd_init_model",
             "wd_free_model", "wd_seq_bytes", "wd_prefill_prompt", "wd_slide_window",
             "wd_refresh_buffer", "wd_step", "wd_full_step", "wd_get_state", "wd_debug_logits",
-            "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error"]
+            "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error", "wd_profile_enable",
+            "wd_profile_read"]
 
 
 class WdError(RuntimeError):
@@ -90,6 +91,9 @@ def _load() -> ctypes.CDLL:
         "wd_free_seq": (None, [P]),
         "wd_plan": (i32, [i32, i32, ctypes.POINTER(WindowConfig), i32, pi32, pi32, pi32, pi32, pi32]),
         "wd_last_error": (ctypes.c_char_p, []),
+        "wd_profile_enable": (i32, [P, i32]),
+        "wd_profile_read": (i32, [P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -309,6 +313,18 @@ def wd_plan(n_prompt: int, gen_len: int, win: WindowConfig):
                                                             ("is_refresh", "ctx_len", "n_active",
                                                              "n_rows", "n_decode")])
     return arrs
+
+
+def wd_profile_enable(model: Model, enable: bool = True) -> None:
+    _check(lib.wd_profile_enable(model.handle, int(bool(enable))))
+
+
+def wd_profile_read(model: Model):
+    """(launches, total_ms, algorithmic bytes, algorithmic flops) since the last read."""
+    n, ms, by, fl = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(lib.wd_profile_read(model.handle, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(by),
+                               ctypes.byref(fl)))
+    return n.value, ms.value, by.value, fl.value
 
 
 def wd_last_error() -> str:

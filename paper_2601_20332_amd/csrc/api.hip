@@ -78,6 +78,10 @@ bool cfg_valid(const wd_model_config* c, std::string* why) {
     *why = "hidden, n_heads*head_dim, ffn and vocab must be multiples of 64";
     return false;
   }
+  if (c->hidden > 16384) {
+    *why = "hidden above 16384 is not supported";
+    return false;
+  }
   if (c->mask_id < 0 || c->mask_id >= c->vocab) {
     *why = "mask_id outside [0, vocab)";
     return false;
@@ -172,6 +176,11 @@ struct wd_model {
   const void* lm;
   std::vector<LayerW> layers;
   int live_seqs = 0;
+  // kernel timing (wd_profile_enable)
+  bool profile = false;
+  std::vector<hipEvent_t> ev;    // event pool, two per recorded launch
+  size_t n_rec = 0;              // launches recorded since the last read
+  std::vector<double> rec_bytes, rec_flops;
 };
 
 namespace {
@@ -346,7 +355,42 @@ wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, 
   return WD_OK;
 }
 
-void wd_free_model(wd_model* m) { delete m; }
+void wd_free_model(wd_model* m) {
+  if (!m) return;
+  for (hipEvent_t e : m->ev) (void)hipEventDestroy(e);
+  delete m;
+}
+
+wd_status wd_profile_enable(wd_model* m, int32_t enable) {
+  if (!m) return fail(WD_ERR_INVALID_ARG, "model is NULL");
+  m->profile = enable != 0;
+  m->n_rec = 0;
+  m->rec_bytes.clear();
+  m->rec_flops.clear();
+  return WD_OK;
+}
+
+wd_status wd_profile_read(wd_model* m, int64_t* launches, double* total_ms, double* alg_bytes,
+                          double* alg_flops) {
+  if (!m) return fail(WD_ERR_INVALID_ARG, "model is NULL");
+  WD_HIP(hipStreamSynchronize(m->stream));
+  double ms = 0.0, by = 0.0, fl = 0.0;
+  for (size_t i = 0; i < m->n_rec; ++i) {
+    float t = 0.f;
+    WD_HIP(hipEventElapsedTime(&t, m->ev[2 * i], m->ev[2 * i + 1]));
+    ms += t;
+    by += m->rec_bytes[i];
+    fl += m->rec_flops[i];
+  }
+  if (launches) *launches = (int64_t)m->n_rec;
+  if (total_ms) *total_ms = ms;
+  if (alg_bytes) *alg_bytes = by;
+  if (alg_flops) *alg_flops = fl;
+  m->n_rec = 0;
+  m->rec_bytes.clear();
+  m->rec_flops.clear();
+  return WD_OK;
+}
 
 }  // extern "C"
 
@@ -367,7 +411,8 @@ struct wd_seq {
   int32_t *x, *seq_len, *row_tok, *row_pos, *row_seq, *row_out, *act_pos, *act_tok, *sel_pos,
       *sel_tok, *err;
   uint8_t *dec, *dec0;
-  float *rope, *h, *C, *logits, *act_conf, *sel_conf, *dbg;
+  float *rope, *h, *C, *logits, *act_conf, *sel_conf, *dbg, *attn_part, *conf_scratch;
+  long attn_part_floats = 0;
   void *kc, *vc, *a, *q, *o, *sw, *a_act;
   long M_max = 0, A_max = 0;
   size_t C_floats = 0;
@@ -380,8 +425,9 @@ namespace {
 struct SeqLayout {
   size_t total = 0;
   size_t x, seq_len, dec, dec0, kc, vc, rope, h, a, q, o, sw, C, row_tok, row_pos, row_seq, row_out,
-      act_pos, act_tok, act_conf, a_act, logits, sel_pos, sel_tok, sel_conf, err, dbg;
-  long M_max, A_max;
+      act_pos, act_tok, act_conf, a_act, logits, sel_pos, sel_tok, sel_conf, err, dbg, attn_part,
+      conf_scratch;
+  long M_max, A_max, attn_part_floats;
   size_t C_floats;
 };
 
@@ -436,6 +482,12 @@ SeqLayout seq_layout(const wd_model& m, const wd_window_config& w, int B, long T
   s.sel_conf = take((size_t)B * w.unmask_per_step * 4);
   s.err = take(4);
   s.dbg = take((size_t)T * c.head_dim * 4);
+  // split-KV partials sized for up to 16 splits of a normal step's rows
+  const long rows_normal = std::min<long>(s.M_max, (long)B * (w.n_active + (long)w.unmask_per_step *
+                                                                           w.refresh_every));
+  s.attn_part_floats = 16L * rows_normal * c.n_heads * (c.head_dim + 2);
+  s.attn_part = take(s.attn_part_floats * 4);
+  s.conf_scratch = take((size_t)3 * s.A_max * wd::kConfChunks * 4);
   s.total = o;
   return s;
 }
@@ -504,16 +556,38 @@ struct Rows {
   WdStepGeom g;
 };
 
+// Event pair around one GEMM launch when kernel timing is on.
+wd_status profile_begin(wd_model& m) {
+  if (!m.profile) return WD_OK;
+  if (m.n_rec >= (1u << 20)) return fail(WD_ERR_OUT_OF_MEMORY, "too many unread timing records");
+  while (m.ev.size() < 2 * (m.n_rec + 1)) {
+    hipEvent_t e;
+    WD_HIP(hipEventCreate(&e));
+    m.ev.push_back(e);
+  }
+  WD_HIP(hipEventRecord(m.ev[2 * m.n_rec], m.stream));
+  return WD_OK;
+}
+
+wd_status profile_end(wd_model& m, int M, int N, int K, size_t esz) {
+  if (!m.profile) return WD_OK;
+  WD_HIP(hipEventRecord(m.ev[2 * m.n_rec + 1], m.stream));
+  m.rec_bytes.push_back((double)N * K * esz + (double)M * K * esz + (double)M * N * 4);
+  m.rec_flops.push_back(2.0 * M * N * K);
+  m.n_rec++;
+  return WD_OK;
+}
+
 template <typename T>
-wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
-               int max_splits, int* splits) {
+wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
+                      int max_splits, int* splits) {
   const wd_model& m = *s->m;
   if (m.cfg.dtype == WD_DTYPE_BF16) {
     wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K);
     if (p.splits > max_splits) {
       p.splits = 1;
       p.ks_per_split = K / 32;
-      p.grid = (N / 32) * ((M + 63) / 64);
+      p.grid = (N / (64 * p.nf)) * ((M + 16 * p.mf - 1) / (16 * p.mf));
     }
     if ((size_t)p.splits * M * N > s->C_floats && C == s->C)
       return fail(WD_ERR_DEVICE, "internal: partial buffer too small");
@@ -524,6 +598,15 @@ wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, i
     *splits = 1;
   }
   return WD_OK;
+}
+
+template <typename T>
+wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
+               int max_splits, int* splits) {
+  wd_model& m = *s->m;
+  WD_TRY(profile_begin(m));
+  WD_TRY(gemm_launch<T>(s, X, ldx, W, C, M, N, K, max_splits, splits));
+  return profile_end(m, M, N, K, m.esz);
 }
 
 template <typename T>
@@ -549,7 +632,8 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
                                c.n_heads, c.n_kv_heads, c.head_dim, q, kc, vc, s->T, st));
     if (c.dtype == WD_DTYPE_BF16) {
       WD_HIP(wd::attention_bf16((const uint16_t*)q, (const uint16_t*)kc, (const uint16_t*)vc, s->T,
-                                (uint16_t*)o, r.g, c.n_heads, c.n_kv_heads, c.head_dim, st));
+                                (uint16_t*)o, r.g, c.n_heads, c.n_kv_heads, c.head_dim,
+                                s->attn_part, s->attn_part_floats, st));
     } else {
       WD_HIP(wd::attention_f32((const float*)q, (const float*)kc, (const float*)vc, s->T,
                                (float*)o, s->row_seq, M, r.g, c.n_heads, c.n_kv_heads, c.head_dim,
@@ -601,7 +685,8 @@ wd_status decide(wd_seq* s, int n_act) {
   else
     WD_TRY(gemm<float>(s, (const float*)s->a_act, c.hidden, m.lm, s->logits, n, c.vocab, c.hidden,
                        1, &S));
-  WD_HIP(wd::confidence(s->logits, n, c.vocab, c.mask_id, s->act_tok, s->act_conf, m.stream));
+  WD_HIP(wd::confidence(s->logits, n, c.vocab, c.mask_id, s->act_tok, s->act_conf, s->conf_scratch,
+                        m.stream));
   const WdStepGeom g = base_geom(s);
   WD_HIP(wd::select_update(s->act_pos, s->act_tok, s->act_conf, n_act, s->win.unmask_per_step, g,
                            s->seq_len, s->x, s->dec, s->sel_pos, s->sel_tok, s->sel_conf, m.stream));
@@ -752,6 +837,9 @@ wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_
   s->sel_conf = (float*)(base + L.sel_conf);
   s->err = (int32_t*)(base + L.err);
   s->dbg = (float*)(base + L.dbg);
+  s->attn_part = (float*)(base + L.attn_part);
+  s->attn_part_floats = L.attn_part_floats;
+  s->conf_scratch = (float*)(base + L.conf_scratch);
   s->M_max = L.M_max;
   s->A_max = L.A_max;
   s->C_floats = L.C_floats;

@@ -11,33 +11,39 @@
 namespace wd {
 
 // ---- confidence: argmax ([MASK] excluded, lowest id on ties) and its softmax probability ----
-__global__ __launch_bounds__(1024) void k_confidence(const float* __restrict__ logits, int V,
-                                                     int mask_id, int32_t* __restrict__ tok,
-                                                     float* __restrict__ conf) {
-  __shared__ float bv[16];
-  __shared__ int bi[16];
-  __shared__ float red[16];
-  const float* L = logits + (long)blockIdx.x * V;
+// Pass 1: block (row, chunk) reduces its slice of the vocabulary to
+// (max, lowest argmax, sum exp(l - max)).  Pass 2: one wave per row merges the
+// chunks in order.  Both passes use fixed reduction orders.
+__device__ __forceinline__ void better(float& bv, int& bi, float ov, int oi) {
+  if (ov > bv || (ov == bv && oi < bi)) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_conf_partial(const float* __restrict__ logits, int V,
+                                                      int mask_id, float* __restrict__ pmax,
+                                                      int* __restrict__ pidx,
+                                                      float* __restrict__ psum) {
+  __shared__ float bv[4], ss[4];
+  __shared__ int bi[4];
+  const int row = blockIdx.x, ch = blockIdx.y;
+  const int per = (V + kConfChunks - 1) / kConfChunks;
+  const int lo = ch * per, hi = min(V, lo + per);
+  const float* L = logits + (long)row * V;
   float best = -INFINITY;
   int idx = INT_MAX;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) {
+  for (int v = lo + threadIdx.x; v < hi; v += blockDim.x) {
     if (v == mask_id) continue;
     const float x = L[v];
-    if (x > best) {  // increasing v: the first maximum is kept
+    if (x > best) {
       best = x;
       idx = v;
     }
   }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ob = __shfl_xor(best, o, 64);
-    const int oi = __shfl_xor(idx, o, 64);
-    if (ob > best || (ob == best && oi < idx)) {
-      best = ob;
-      idx = oi;
-    }
-  }
-  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int o = 32; o > 0; o >>= 1) better(best, idx, __shfl_xor(best, o, 64), __shfl_xor(idx, o, 64));
+  const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
     bv[w] = best;
     bi[w] = idx;
@@ -45,25 +51,51 @@ __global__ __launch_bounds__(1024) void k_confidence(const float* __restrict__ l
   __syncthreads();
   best = bv[0];
   idx = bi[0];
-  for (int i = 1; i < nw; ++i)
-    if (bv[i] > best || (bv[i] == best && bi[i] < idx)) {
-      best = bv[i];
-      idx = bi[i];
-    }
+  for (int i = 1; i < 4; ++i) better(best, idx, bv[i], bi[i]);
   float s = 0.f;
-  for (int v = threadIdx.x; v < V; v += blockDim.x)
-    if (v != mask_id) s += expf(L[v] - best);
-  s = block_sum(s, red);
+  if (best > -INFINITY)
+    for (int v = lo + threadIdx.x; v < hi; v += blockDim.x)
+      if (v != mask_id) s += expf(L[v] - best);
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) ss[w] = s;
+  __syncthreads();
   if (threadIdx.x == 0) {
-    tok[blockIdx.x] = idx;
-    conf[blockIdx.x] = 1.0f / s;
+    const int k = row * kConfChunks + ch;
+    pmax[k] = best;
+    pidx[k] = idx;
+    psum[k] = ss[0] + ss[1] + ss[2] + ss[3];
   }
 }
 
+__global__ __launch_bounds__(64) void k_conf_final(const float* __restrict__ pmax,
+                                                   const int* __restrict__ pidx,
+                                                   const float* __restrict__ psum,
+                                                   int32_t* __restrict__ tok,
+                                                   float* __restrict__ conf) {
+  const int row = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  float best = -INFINITY;
+  int idx = INT_MAX;
+  for (int c = 0; c < kConfChunks; ++c)
+    better(best, idx, pmax[row * kConfChunks + c], pidx[row * kConfChunks + c]);
+  float s = 0.f;
+  for (int c = 0; c < kConfChunks; ++c) {
+    const float m = pmax[row * kConfChunks + c];
+    if (m > -INFINITY) s += psum[row * kConfChunks + c] * expf(m - best);
+  }
+  tok[row] = idx;
+  conf[row] = 1.0f / s;
+}
+
 hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* tok, float* conf,
-                      hipStream_t st) {
+                      float* scratch, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_confidence, dim3(n), dim3(1024), 0, st, logits, V, mask_id, tok, conf);
+  float* pmax = scratch;
+  int* pidx = (int*)(scratch + (long)n * kConfChunks);
+  float* psum = scratch + 2L * n * kConfChunks;
+  hipLaunchKernelGGL(k_conf_partial, dim3(n, kConfChunks), dim3(256), 0, st, logits, V, mask_id,
+                     pmax, pidx, psum);
+  hipLaunchKernelGGL(k_conf_final, dim3(n), dim3(64), 0, st, pmax, pidx, psum, tok, conf);
   return hipGetLastError();
 }
 

@@ -43,17 +43,29 @@ hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st
 }
 
 // ---- bf16 weight-streaming GEMM ----------------------------------------------------
-// Workgroup = 4 waves on the same NF 16-row weight groups and the same
-// 16*MF activation rows; the waves take every 4th 32-wide K step of the
-// workgroup's split and are summed through LDS at the end.
-// Grid = NB (weight groups / NF) x MT (row tiles) x S (K splits), remapped so
-// that each XCD receives a contiguous range of tiles (row tiles of one weight
-// group share an L2).
-template <int NF, int MF>
+// Workgroup = 4 waves; wave w owns NF 16-row weight groups (the workgroup
+// covers 64*NF output features), all four waves walk the same K range.  The
+// activation rows of the tile (16*MF rows) are staged through LDS in chunks
+// of CK 32-wide K steps, so each activation fragment is fetched from L2 once
+// per workgroup and read by all four waves; the next chunk is prefetched
+// into registers while the current one is consumed.  Weights go straight
+// from HBM to registers (non-temporal), U K steps ahead of the MFMAs.
+// Grid = NB (weight groups / (4 NF)) x MT (row tiles) x S (K splits),
+// remapped so that each XCD receives a contiguous range of tiles (the row
+// tiles and splits of one weight group share an L2).
+constexpr int kWaves = 4;
+constexpr int kCK = 8;
+
+template <int NF, int MF, int U>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ X, int ldx,
                                                    const u32x4* __restrict__ Wp,
                                                    float* __restrict__ C, int M, int N, int K,
                                                    int NB, int MT, int S, int ks_per_split) {
+  constexpr int ROWS = 16 * MF;
+  constexpr int PITCH = kCK * 32 + 8;   // bf16 per LDS row; the 16-byte pad spreads banks
+  constexpr int CHUNK16 = ROWS * kCK * 4;
+  constexpr int PER_T = (CHUNK16 + 255) / 256;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[ROWS * PITCH];
   const int G = NB * MT * S;
   int id = blockIdx.x;
   if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);
@@ -61,113 +73,128 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
   const int rest = id / MT;
   const int nb = rest % NB;
   const int s = rest / NB;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int KT = K >> 5;
   const int kt0 = s * ks_per_split;
   const int kt1 = min(KT, kt0 + ks_per_split);
-  const int m0 = mt * 16 * MF;
-
+  const int m0 = mt * ROWS;
+  const int f0 = (nb * kWaves + wave) * NF;
   const u32x4* wp[NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) wp[f] = Wp + ((long)(nb * NF + f) * KT) * 64 + lane;
-  const uint16_t* xp[MF];
-  bool xv[MF];
-#pragma unroll
-  for (int f = 0; f < MF; ++f) {
-    const int row = m0 + f * 16 + (lane & 15);
-    xv[f] = row < M;
-    xp[f] = X + (long)(xv[f] ? row : 0) * ldx + (lane >> 4) * 8;
-  }
-
+  for (int f = 0; f < NF; ++f) wp[f] = Wp + ((long)(f0 + f) * KT) * 64 + lane;
   f32x4 acc[NF][MF];
 #pragma unroll
   for (int a = 0; a < NF; ++a)
 #pragma unroll
     for (int b = 0; b < MF; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   const u32x4 zero = {0u, 0u, 0u, 0u};
-  int kt = kt0 + wave;
-  // Four K steps per iteration: all loads first, so each wave keeps
-  // 4 * (NF + MF) 16-byte loads in flight.
-  for (; kt + 12 < kt1; kt += 16) {
-    u32x4 a[4][NF], b[4][MF];
+  const int nchunk = (kt1 - kt0 + kCK - 1) / kCK;
+  u32x4 pre[PER_T];
+  // chunk c of the tile's activations: rows m0.., K steps kt0 + c*kCK ..; rows >= M
+  // and K steps >= kt1 read as zero
+  auto gload = [&](int c) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-#pragma unroll
-      for (int f = 0; f < NF; ++f) a[u][f] = __builtin_nontemporal_load(wp[f] + (long)(kt + 4 * u) * 64);
-#pragma unroll
-      for (int f = 0; f < MF; ++f)
-        b[u][f] = xv[f] ? *(const u32x4*)(xp[f] + (kt + 4 * u) * 32) : zero;
+    for (int i = 0; i < PER_T; ++i) {
+      const int e = tid + i * 256;
+      pre[i] = zero;
+      if (e < CHUNK16) {
+        const int r = e / (kCK * 4), cc = e % (kCK * 4);
+        const int kt = kt0 + c * kCK + cc / 4;
+        if (m0 + r < M && kt < kt1) pre[i] = *(const u32x4*)(X + (long)(m0 + r) * ldx + kt * 32 + (cc & 3) * 8);
+      }
     }
+  };
+  auto lstore = [&]() {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int i = 0; i < PER_T; ++i) {
+      const int e = tid + i * 256;
+      if (e < CHUNK16) {
+        const int r = e / (kCK * 4), cc = e % (kCK * 4);
+        *(u32x4*)(&xs[r * PITCH + cc * 8]) = pre[i];
+      }
+    }
+  };
+  gload(0);
+  lstore();
+  __syncthreads();
+  for (int c = 0; c < nchunk; ++c) {
+    if (c + 1 < nchunk) gload(c + 1);
+    const int kbase = kt0 + c * kCK;
+    const int nk = min(kCK, kt1 - kbase);
+    for (int k = 0; k < nk; k += U) {
+      u32x4 a[U][NF];
 #pragma unroll
-      for (int i = 0; i < NF; ++i)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int j = 0; j < MF; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, a[u][i]), __builtin_bit_cast(bf16x8, b[u][j]), acc[i][j],
-              0, 0, 0);
+        for (int f = 0; f < NF; ++f)
+          a[u][f] = (k + u < nk) ? __builtin_nontemporal_load(wp[f] + (long)(kbase + k + u) * 64) : zero;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        u32x4 b[MF];
+#pragma unroll
+        for (int f = 0; f < MF; ++f)
+          b[f] = *(const u32x4*)(&xs[(f * 16 + (lane & 15)) * PITCH + (k + u) * 32 + (lane >> 4) * 8]);
+#pragma unroll
+        for (int i = 0; i < NF; ++i)
+#pragma unroll
+          for (int j = 0; j < MF; ++j) acc[i][j] = mfma16(a[u][i], b[j], acc[i][j]);
+      }
+    }
+    if (c + 1 < nchunk) {
+      __syncthreads();
+      lstore();
+      __syncthreads();
+    }
   }
-  for (; kt < kt1; kt += 4) {
-    u32x4 a[NF], b[MF];
-#pragma unroll
-    for (int f = 0; f < NF; ++f) a[f] = __builtin_nontemporal_load(wp[f] + (long)kt * 64);
-#pragma unroll
-    for (int f = 0; f < MF; ++f) b[f] = xv[f] ? *(const u32x4*)(xp[f] + kt * 32) : zero;
-#pragma unroll
-    for (int i = 0; i < NF; ++i)
-#pragma unroll
-      for (int j = 0; j < MF; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, a[i]), __builtin_bit_cast(bf16x8, b[j]), acc[i][j], 0, 0, 0);
-  }
-
-  __shared__ f32x4 red[4][NF * MF][64];
 #pragma unroll
   for (int i = 0; i < NF; ++i)
 #pragma unroll
-    for (int j = 0; j < MF; ++j) red[wave][i * MF + j][lane] = acc[i][j];
-  __syncthreads();
-  for (int o = threadIdx.x; o < NF * MF * 64; o += 256) {
-    const int f = o >> 6, l = o & 63;
-    const int i = f / MF, j = f % MF;
-    const int m = m0 + j * 16 + (l & 15);
-    if (m >= M) continue;
-    f32x4 v = red[0][f][l];
-    v += red[1][f][l];
-    v += red[2][f][l];
-    v += red[3][f][l];
-    const int n = (nb * NF + i) * 16 + (l >> 4) * 4;
-    *(f32x4*)(C + ((long)s * M + m) * N + n) = v;
-  }
+    for (int j = 0; j < MF; ++j) {
+      const int m = m0 + j * 16 + (lane & 15);
+      if (m < M) *(f32x4*)(C + ((long)s * M + m) * N + (f0 + i) * 16 + (lane >> 4) * 4) = acc[i][j];
+    }
 }
 
-constexpr int kNF = 2;
-constexpr int kMF = 4;
-
+// Launch shape: weight groups per wave (NF), activation fragments per tile
+// (MF) and K splits, from the measured behaviour of the kernel on MI355X:
+// wide matrices (N >= 16384) stream best with 2 groups per wave and as few
+// splits as give >= 384 workgroups; narrower ones with 1 group per wave and
+// >= 512 workgroups.
 GemmPlan plan_gemm_bf16(int M, int N, int K) {
   GemmPlan p;
-  const int NB = N / (16 * kNF);
-  const int MT = (M + 16 * kMF - 1) / (16 * kMF);
+  p.nf = (N >= 16384 && N % 128 == 0) ? 2 : 1;
+  p.mf = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
+  const int NB = N / (16 * kWaves * p.nf);
+  const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
   const int KT = K / 32;
+  const long target = p.nf == 2 ? 384 : 512;
   int S = 1;
-  // enough workgroups to cover every CU twice, while each wave keeps >= 4 K steps
-  while ((long)NB * MT * S < 512 && KT / (2 * S) >= 16) S *= 2;
-  p.splits = S;
+  while ((long)NB * MT * S < target && KT / (2 * S) >= kCK) S *= 2;
   p.ks_per_split = (KT + S - 1) / S;
   p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
   p.grid = NB * MT * p.splits;
   return p;
 }
 
+template <int NF, int MF>
+static void launch_mf(dim3 grid, hipStream_t st, const uint16_t* X, int ldx, const void* Wp,
+                      float* C, int M, int N, int K, int NB, int MT, int S, int ks) {
+  hipLaunchKernelGGL((k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4>), grid, dim3(256), 0, st, X, ldx,
+                     (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks);
+}
+
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
                      const GemmPlan& p, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  const int NB = N / (16 * kNF);
-  const int MT = (M + 16 * kMF - 1) / (16 * kMF);
-  hipLaunchKernelGGL((k_gemm_bf16<kNF, kMF>), dim3(p.grid), dim3(256), 0, st, X, ldx,
-                     (const u32x4*)Wp, C, M, N, K, NB, MT, p.splits, p.ks_per_split);
+  const int NB = N / (16 * kWaves * p.nf);
+  const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
+  if (NB * MT * p.splits != p.grid || N % (16 * kWaves * p.nf) || K % 32) return hipErrorInvalidValue;
+  const dim3 grid(p.grid);
+#define WD_GEMM_CASE(NF, MF) \
+  if (p.nf == NF && p.mf == MF) launch_mf<NF, MF>(grid, st, X, ldx, Wp, C, M, N, K, NB, MT, p.splits, p.ks_per_split);
+  WD_GEMM_CASE(1, 1) WD_GEMM_CASE(1, 2) WD_GEMM_CASE(1, 3) WD_GEMM_CASE(1, 4)
+  WD_GEMM_CASE(2, 1) WD_GEMM_CASE(2, 2) WD_GEMM_CASE(2, 3) WD_GEMM_CASE(2, 4)
+#undef WD_GEMM_CASE
   return hipGetLastError();
 }
 

@@ -13,6 +13,8 @@ namespace wd {
 
 // ---- GEMM (gemm.hip) -------------------------------------------------------------
 struct GemmPlan {
+  int nf = 1;            // 16-row weight groups per wave
+  int mf = 4;            // 16-row activation fragments per row tile
   int splits = 1;        // K splits = number of partial outputs
   int ks_per_split = 0;  // 32-wide K steps per split
   int grid = 0;
@@ -45,16 +47,21 @@ template <typename T>
 hipError_t swiglu(const float* C, int S, int M, int F, T* out, hipStream_t st);
 // Non-causal attention of the step's rows over cache rows [0, c) of their
 // sequence (rows of sequence b are g.row0[b] .. g.row0[b] + g.nrows[b] - 1).
+// `part` (part_floats floats) holds split-KV partials; fewer splits are used
+// when it is too small.
 hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint16_t* vcache,
                           long cache_rows, uint16_t* o, const WdStepGeom& g, int n_heads, int n_kv,
-                          int head_dim, hipStream_t st);
+                          int head_dim, float* part, long part_floats, hipStream_t st);
 hipError_t attention_f32(const float* q, const float* kcache, const float* vcache, long cache_rows,
                          float* o, const int32_t* row_seq, int M, const WdStepGeom& g, int n_heads,
                          int n_kv, int head_dim, hipStream_t st);
 
 // ---- decisions and bookkeeping (decide.hip) -------------------------------------------
+// Two passes: kConfChunks vocabulary chunks per row into `scratch`
+// (3 * n * kConfChunks floats), then a per-row combine.
+constexpr int kConfChunks = 16;
 hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* tok, float* conf,
-                      hipStream_t st);
+                      float* scratch, hipStream_t st);
 // Row set of a step.  mode 0 = refresh ([0, c) of each sequence), 1 = normal
 // (active + phase-decoded positions), 2 = full ([0, S) of each sequence,
 // every undecoded position active).  Active rows of sequence b get compact

@@ -11,65 +11,95 @@
 namespace wd {
 
 // ---- embedding gather + first RMSNorm ------------------------------------------------
+// One block per row, 1024 threads; H must be a multiple of 4 and at most 16384.
 template <typename T>
-__global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ x,
-                                                    const int32_t* __restrict__ row_tok,
-                                                    const T* __restrict__ emb,
-                                                    const T* __restrict__ gamma, float eps,
-                                                    float* __restrict__ h, T* __restrict__ a, int H) {
+__global__ __launch_bounds__(1024) void k_embed_norm(const int32_t* __restrict__ x,
+                                                     const int32_t* __restrict__ row_tok,
+                                                     const T* __restrict__ emb,
+                                                     const T* __restrict__ gamma, float eps,
+                                                     float* __restrict__ h, T* __restrict__ a, int H) {
   __shared__ float red[16];
   const long r = blockIdx.x;
   const T* e = emb + (long)x[row_tok[r]] * H;
   float* hr = h + r * H;
+  float v[4][4];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    const float v = Elem<T>::load(e + i);
-    hr[i] = v;
-    ss += v * v;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int i = (threadIdx.x + it * 1024) * 4;
+    if (i < H) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[it][q] = Elem<T>::load(e + i + q);
+        ss += v[it][q] * v[it][q];
+      }
+      *(f32x4*)(hr + i) = f32x4{v[it][0], v[it][1], v[it][2], v[it][3]};
+    }
   }
   const float inv = 1.0f / sqrtf(block_sum(ss, red) / (float)H + eps);
-  for (int i = threadIdx.x; i < H; i += blockDim.x)
-    a[r * H + i] = Elem<T>::from_f(hr[i] * inv * Elem<T>::load(gamma + i));
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int i = (threadIdx.x + it * 1024) * 4;
+    if (i < H)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        a[r * H + i + q] = Elem<T>::from_f(v[it][q] * inv * Elem<T>::load(gamma + i + q));
+  }
 }
 
 template <typename T>
 hipError_t embed_norm(const int32_t* x, const int32_t* row_tok, const T* emb, const T* gamma,
                       float eps, float* h, T* a, int M, int H, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_embed_norm<T>, dim3(M), dim3(256), 0, st, x, row_tok, emb, gamma, eps, h, a, H);
+  if (H % 4 || H > 16384) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_embed_norm<T>, dim3(M), dim3(1024), 0, st, x, row_tok, emb, gamma, eps, h, a, H);
   return hipGetLastError();
 }
 
 // ---- residual add of split-K partials + RMSNorm -----------------------------------------
+// One block per row, 1024 threads, 4 consecutive features per thread and pass,
+// so every partial of the row is in flight at once.
 template <typename T>
-__global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
-                                                       const float* __restrict__ C, int S, int M,
-                                                       int H, const T* __restrict__ gamma,
-                                                       float eps, T* __restrict__ a,
-                                                       const int32_t* __restrict__ row_out) {
+__global__ __launch_bounds__(1024) void k_residual_norm(float* __restrict__ h,
+                                                        const float* __restrict__ C, int S, int M,
+                                                        int H, const T* __restrict__ gamma,
+                                                        float eps, T* __restrict__ a,
+                                                        const int32_t* __restrict__ row_out) {
   __shared__ float red[16];
   const long r = blockIdx.x;
   float* hr = h + r * H;
+  f32x4 v[4];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    float acc = 0.f;
-    for (int s = 0; s < S; ++s) acc += C[((long)s * M + r) * H + i];
-    const float v = hr[i] + acc;
-    hr[i] = v;
-    ss += v * v;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int i = (threadIdx.x + it * 1024) * 4;
+    if (i < H) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < S; ++s) acc += *(const f32x4*)(C + ((long)s * M + r) * H + i);
+      v[it] = *(const f32x4*)(hr + i) + acc;
+      *(f32x4*)(hr + i) = v[it];
+      ss += v[it][0] * v[it][0] + v[it][1] * v[it][1] + v[it][2] * v[it][2] + v[it][3] * v[it][3];
+    }
   }
   const int dst = row_out ? row_out[r] : (int)r;
   if (dst < 0) return;  // uniform over the block
   const float inv = 1.0f / sqrtf(block_sum(ss, red) / (float)H + eps);
-  for (int i = threadIdx.x; i < H; i += blockDim.x)
-    a[(long)dst * H + i] = Elem<T>::from_f(hr[i] * inv * Elem<T>::load(gamma + i));
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int i = (threadIdx.x + it * 1024) * 4;
+    if (i < H)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        a[(long)dst * H + i + q] = Elem<T>::from_f(v[it][q] * inv * Elem<T>::load(gamma + i + q));
+  }
 }
 
 template <typename T>
 hipError_t residual_norm(float* h, const float* C, int S, int M, int H, const T* gamma, float eps,
                          T* a, const int32_t* row_out, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_residual_norm<T>, dim3(M), dim3(256), 0, st, h, C, S, M, H, gamma, eps, a,
+  if (H % 4 || H > 16384) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_residual_norm<T>, dim3(M), dim3(1024), 0, st, h, C, S, M, H, gamma, eps, a,
                      row_out);
   return hipGetLastError();
 }
@@ -212,17 +242,26 @@ constexpr int kKT = 64;              // keys per tile
 constexpr int kKPitch = kAttD + 8;   // bf16 elements per K row in LDS
 constexpr int kVPitch = kKT + 8;     // bf16 elements per V^T row in LDS
 
+// Split-KV: blockIdx.z = query block * nsplit + split; split s covers keys
+// [s * keys_per_split, (s + 1) * keys_per_split) of [0, c).  With nsplit == 1
+// the normalized output is written as bf16; otherwise the unnormalized fp32
+// output and the running max / sum go to part / ml for k_attn_combine.
 __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ q,
                                                    const uint16_t* __restrict__ kc,
                                                    const uint16_t* __restrict__ vc,
                                                    long cache_rows, uint16_t* __restrict__ o,
-                                                   WdStepGeom g, int nh, int nkv) {
+                                                   WdStepGeom g, int nh, int nkv, int nsplit,
+                                                   int keys_per_split, int M,
+                                                   float* __restrict__ part,
+                                                   float* __restrict__ ml) {
   __shared__ __attribute__((aligned(16))) uint16_t Ks[kKT * kKPitch];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[kAttD * kVPitch];
-  const int h = blockIdx.x, b = blockIdx.y, qb = blockIdx.z;
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int qb = blockIdx.z / nsplit, split = blockIdx.z % nsplit;
   const int nq = g.nrows[b];
   if (qb * 64 >= nq) return;
-  const int c = g.ctx[b];
+  const int key_lo = split * keys_per_split;
+  const int c = min(g.ctx[b], key_lo + keys_per_split);
   const long off = g.off[b];
   const int row0 = g.row0[b];
   const int kvh = h / (nh / nkv);
@@ -248,7 +287,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
   float m_run = -INFINITY, l_run = 0.f;
   const float scale = 0.08838834764831845f;  // 1/sqrt(128)
 
-  for (int j0 = 0; j0 < c; j0 += kKT) {
+  for (int j0 = key_lo; j0 < c; j0 += kKT) {
     __syncthreads();
     // K tile: 64 rows x 256 B; V tile transposed into Vt[dd][key]
     for (int e = tid; e < kKT * 16; e += 256) {
@@ -335,6 +374,17 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
     }
   }
   if (!qvalid) return;
+  if (nsplit > 1) {
+    const long pr = ((long)split * M + row0 + qi) * nh + h;
+    float* prow = part + pr * kAttD;
+#pragma unroll
+    for (int df = 0; df < 8; ++df) *(f32x4*)(prow + df * 16 + grp * 4) = oacc[df];
+    if (grp == 0) {
+      ml[pr * 2] = m_run;
+      ml[pr * 2 + 1] = l_run;
+    }
+    return;
+  }
   const float inv = 1.0f / l_run;
   uint16_t* orow = o + (long)(row0 + qi) * ldq + h * kAttD;
 #pragma unroll
@@ -346,16 +396,50 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
   }
 }
 
+// out = sum_s exp(m_s - m) O_s / sum_s exp(m_s - m) l_s, m = max_s m_s
+__global__ __launch_bounds__(128) void k_attn_combine(const float* __restrict__ part,
+                                                      const float* __restrict__ ml, int nsplit,
+                                                      int M, int nh, uint16_t* __restrict__ o) {
+  const int r = blockIdx.x, h = blockIdx.y, dd = threadIdx.x;
+  float mx = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, ml[(((long)s * M + r) * nh + h) * 2]);
+  float l = 0.f, acc = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const long pr = ((long)s * M + r) * nh + h;
+    const float w = expf(ml[pr * 2] - mx);
+    l += w * ml[pr * 2 + 1];
+    acc += w * part[pr * kAttD + dd];
+  }
+  o[((long)r * nh + h) * kAttD + dd] = f2bf(acc / l);
+}
+
 hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint16_t* vcache,
                           long cache_rows, uint16_t* o, const WdStepGeom& g, int n_heads, int n_kv,
-                          int head_dim, hipStream_t st) {
+                          int head_dim, float* part, long part_floats, hipStream_t st) {
   if (head_dim != kAttD) return hipErrorInvalidValue;
-  int nqmax = 0;
-  for (int b = 0; b < g.batch; ++b) nqmax = std::max(nqmax, g.nrows[b]);
+  int nqmax = 0, cmax = 0, M = 0;
+  long qblocks = 0;
+  for (int b = 0; b < g.batch; ++b) {
+    nqmax = std::max(nqmax, g.nrows[b]);
+    cmax = std::max(cmax, g.ctx[b]);
+    M = std::max(M, g.row0[b] + g.nrows[b]);
+    qblocks += (g.nrows[b] + 63) / 64;
+  }
   if (nqmax <= 0) return hipSuccess;
-  dim3 grid(n_heads, g.batch, (nqmax + 63) / 64);
+  // split the keys until about 512 workgroups run, if the partial buffer allows
+  const int tiles = (cmax + kKT - 1) / kKT;
+  int nsplit = std::min<long>(tiles, std::max<long>(1, (512 + n_heads * qblocks - 1) / (n_heads * qblocks)));
+  nsplit = std::min(nsplit, 16);
+  while (nsplit > 1 && (long)nsplit * M * n_heads * (kAttD + 2) > part_floats) --nsplit;
+  const int tps = (tiles + nsplit - 1) / nsplit;
+  nsplit = (tiles + tps - 1) / tps;
+  float* ml = part + (long)nsplit * M * n_heads * kAttD;
+  dim3 grid(n_heads, g.batch, ((nqmax + 63) / 64) * nsplit);
   hipLaunchKernelGGL(k_attn_bf16, grid, dim3(256), 0, st, q, kcache, vcache, cache_rows, o, g,
-                     n_heads, n_kv);
+                     n_heads, n_kv, nsplit, tps * kKT, M, part, ml);
+  if (nsplit > 1)
+    hipLaunchKernelGGL(k_attn_combine, dim3(M, n_heads), dim3(kAttD), 0, st, part, ml, nsplit, M,
+                       n_heads, o);
   return hipGetLastError();
 }
 
