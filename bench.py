@@ -146,7 +146,7 @@ def main():
     ap.add_argument("--steps", type=int, default=3, help="timed whole generations")
     ap.add_argument("--warmup", type=int, default=1, help="untimed whole generations")
     ap.add_argument("--workload", default="llada8b",
-                    choices=["llada8b", "dream7b", "llada8b_long"])
+                    choices=["llada8b", "dream7b", "llada8b_long", "llada8b_batch16"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full", action="store_true", help="skip the full-sequence comparison")
     ap.add_argument("--no-events", action="store_true",

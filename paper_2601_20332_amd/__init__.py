@@ -284,9 +284,13 @@ def wd_get_state(gen: Generation):
 
 
 def wd_debug_logits(gen: Generation):
-    cap = gen.batch * max(gen.lens)
     V = gen.model.cfg.vocab
     n = ctypes.c_int32()
+    probe = np.empty(1, np.float32)
+    st = lib.wd_debug_logits(gen.handle, _f32p(probe), None, 0, ctypes.byref(n))
+    if st not in (WD_OK, WD_ERR_OUT_OF_MEMORY):
+        _check(st)
+    cap = max(1, n.value)
     logits = np.empty((cap, V), np.float32)
     pos = np.empty(cap, np.int32)
     _check(lib.wd_debug_logits(gen.handle, _f32p(logits), _i32p(pos), cap, ctypes.byref(n)))

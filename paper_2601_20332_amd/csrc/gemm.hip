@@ -54,9 +54,8 @@ hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st
 // remapped so that each XCD receives a contiguous range of tiles (the row
 // tiles and splits of one weight group share an L2).
 constexpr int kWaves = 4;
-constexpr int kCK = 8;
 
-template <int NF, int MF, int U>
+template <int NF, int MF, int U, int kCK>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ X, int ldx,
                                                    const u32x4* __restrict__ Wp,
                                                    float* __restrict__ C, int M, int N, int K,
@@ -104,7 +103,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
       }
     }
   };
-  auto lstore = [&]() {
+  auto lstore = [&](int c) {
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
       const int e = tid + i * 256;
@@ -115,7 +114,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     }
   };
   gload(0);
-  lstore();
+  lstore(0);
   __syncthreads();
   for (int c = 0; c < nchunk; ++c) {
     if (c + 1 < nchunk) gload(c + 1);
@@ -142,7 +141,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     }
     if (c + 1 < nchunk) {
       __syncthreads();
-      lstore();
+      lstore(c + 1);
       __syncthreads();
     }
   }
@@ -155,21 +154,157 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     }
 }
 
-// Launch shape: weight groups per wave (NF), activation fragments per tile
-// (MF) and K splits, from the measured behaviour of the kernel on MI355X:
-// wide matrices (N >= 16384) stream best with 2 groups per wave and as few
-// splits as give >= 384 workgroups; narrower ones with 1 group per wave and
-// >= 512 workgroups.
+
+// ---- bf16 GEMM for many rows (refresh steps, the full-sequence path, batches) ----------
+// Same operands and tile order as above, with 128-row activation tiles and
+// NF weight groups per wave (16*NF*8 MFMAs per 4 K steps).  With few waves per
+// CU, load latency must be covered by loads in flight: weights are fetched
+// two iterations (8 K steps) ahead through a ring of three register buffers,
+// the next activation chunk one iteration ahead into the other half of a
+// double-buffered LDS tile; one barrier per iteration.
+template <int NF>
+__global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __restrict__ X, int ldx,
+                                                          const u32x4* __restrict__ Wp,
+                                                          float* __restrict__ C, int M, int N,
+                                                          int K, int NB, int MT, int S,
+                                                          int ks_per_split) {
+  constexpr int MF = 8, U = 4;
+  constexpr int ROWS = 16 * MF;
+  constexpr int PITCH = U * 32 + 8;
+  constexpr int CHUNK16 = ROWS * U * 4;
+  constexpr int PER_T = CHUNK16 / 256;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][ROWS * PITCH];
+  const int G = NB * MT * S;
+  int id = blockIdx.x;
+  if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);
+  const int mt = id % MT;
+  const int rest = id / MT;
+  const int nb = rest % NB;
+  const int s = rest / NB;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int KT = K >> 5;
+  const int kt0 = s * ks_per_split;
+  const int kt1 = min(KT, kt0 + ks_per_split);
+  const int m0 = mt * ROWS;
+  const int f0 = (nb * kWaves + wave) * NF;
+  const u32x4* wp[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) wp[f] = Wp + ((long)(f0 + f) * KT) * 64 + lane;
+  f32x4 acc[NF][MF];
+#pragma unroll
+  for (int a = 0; a < NF; ++a)
+#pragma unroll
+    for (int b = 0; b < MF; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  const int n_it = (kt1 - kt0 + U - 1) / U;
+  u32x4 pre[PER_T];
+  u32x4 a0[U][NF], a1[U][NF], a2[U][NF];
+
+  // Loads are branch-free and never waited on early: an out-of-range K step
+  // reads the weights of the last valid step (finite values, multiplied by
+  // the zero activations stored for that step), and out-of-range activation
+  // elements read a clamped address and are zeroed only when they are
+  // stored to LDS.
+  auto wload = [&](u32x4 (&a)[U][NF], int it) {
+    const int kb = kt0 + it * U;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kk = min(kb + u, kt1 - 1);
+#pragma unroll
+      for (int f = 0; f < NF; ++f) a[u][f] = __builtin_nontemporal_load(wp[f] + (long)kk * 64);
+    }
+  };
+  auto xload = [&](int it) {
+    const int kb = kt0 + it * U;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int e = tid + i * 256;
+      const int r = e / (U * 4), cc = e % (U * 4);
+      const long row = min(m0 + r, M - 1);
+      const int kc = min(kb + cc / 4, kt1 - 1);
+      pre[i] = *(const u32x4*)(X + row * ldx + kc * 32 + (cc & 3) * 8);
+    }
+  };
+  auto xstore = [&](int buf, int it) {
+    const int kb = kt0 + it * U;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int e = tid + i * 256;
+      const int r = e / (U * 4), cc = e % (U * 4);
+      const bool ok = m0 + r < M && kb + cc / 4 < kt1;
+      *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[i] : zero;
+    }
+  };
+  auto compute = [&](const u32x4 (&a)[U][NF], int buf) {
+    const uint16_t* xb = xs[buf];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      u32x4 b[MF];
+#pragma unroll
+      for (int j = 0; j < MF; ++j)
+        b[j] = *(const u32x4*)(&xb[(j * 16 + (lane & 15)) * PITCH + u * 32 + (lane >> 4) * 8]);
+#pragma unroll
+      for (int j = 0; j < MF; ++j)
+#pragma unroll
+        for (int i = 0; i < NF; ++i) acc[i][j] = mfma16(a[u][i], b[j], acc[i][j]);
+    }
+  };
+  // iteration it: weights of it come from `cur`, weights of it + 2 go to `ld`
+  // The activation loads go first: the load counter is in order, so waiting
+  // for them before the LDS store must not also wait for the weight prefetch.
+  auto body = [&](u32x4 (&cur)[U][NF], u32x4 (&ld)[U][NF], int it) {
+    const bool more = it + 1 < n_it;
+    if (more) xload(it + 1);
+    if (it + 2 < n_it) wload(ld, it + 2);
+    compute(cur, it & 1);
+    if (more) xstore((it + 1) & 1, it + 1);
+    __syncthreads();
+  };
+
+  xload(0);
+  wload(a0, 0);
+  if (n_it > 1) wload(a1, 1);
+  xstore(0, 0);
+  __syncthreads();
+  for (int it = 0; it < n_it; it += 3) {
+    body(a0, a2, it);
+    if (it + 1 < n_it) body(a1, a0, it + 1);
+    if (it + 2 < n_it) body(a2, a1, it + 2);
+  }
+#pragma unroll
+  for (int i = 0; i < NF; ++i)
+#pragma unroll
+    for (int j = 0; j < MF; ++j) {
+      const int m = m0 + j * 16 + (lane & 15);
+      if (m < M) *(f32x4*)(C + ((long)s * M + m) * N + (f0 + i) * 16 + (lane >> 4) * 4) = acc[i][j];
+    }
+}
+
+// Launch shape, from the measured behaviour of the kernel on MI355X.
+// Up to 64 rows (normal steps, weight-streaming bound): one row tile of
+// 16*MF rows; wide matrices (N >= 16384) stream best with 2 weight groups
+// per wave and as few K splits as give >= 384 workgroups, narrower ones with
+// 1 group per wave and >= 512 workgroups.  Above 64 rows (refresh steps, the
+// full-sequence path, batches): 128-row tiles and 2 weight groups per wave
+// (16 MFMAs per 16-byte weight load), software-pipelined, with K splits only
+// until 256 workgroups run (split-K partials cost rows*N*4 bytes each).
 GemmPlan plan_gemm_bf16(int M, int N, int K) {
   GemmPlan p;
-  p.nf = (N >= 16384 && N % 128 == 0) ? 2 : 1;
-  p.mf = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
+  const int KT = K / 32;
+  if (M <= 64) {
+    p.nf = (N >= 16384 && N % 128 == 0) ? 2 : 1;
+    p.mf = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
+    p.ck = 8;
+  } else {
+    p.mf = 8;
+    p.ck = 4;
+    p.nf = N % 128 == 0 ? 2 : 1;
+  }
   const int NB = N / (16 * kWaves * p.nf);
   const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
-  const int KT = K / 32;
-  const long target = p.nf == 2 ? 384 : 512;
+  const long target = M > 64 ? 256 : p.nf == 2 ? 384 : 512;
   int S = 1;
-  while ((long)NB * MT * S < target && KT / (2 * S) >= kCK) S *= 2;
+  while ((long)NB * MT * S < target && KT / (2 * S) >= p.ck) S *= 2;
   p.ks_per_split = (KT + S - 1) / S;
   p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
   p.grid = NB * MT * p.splits;
@@ -179,8 +314,13 @@ GemmPlan plan_gemm_bf16(int M, int N, int K) {
 template <int NF, int MF>
 static void launch_mf(dim3 grid, hipStream_t st, const uint16_t* X, int ldx, const void* Wp,
                       float* C, int M, int N, int K, int NB, int MT, int S, int ks) {
-  hipLaunchKernelGGL((k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4>), grid, dim3(256), 0, st, X, ldx,
-                     (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks);
+  if constexpr (MF == 8) {
+    hipLaunchKernelGGL((k_gemm_bf16_big<NF>), grid, dim3(256), 0, st, X, ldx, (const u32x4*)Wp, C,
+                       M, N, K, NB, MT, S, ks);
+  } else {
+    hipLaunchKernelGGL((k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4, 8>), grid, dim3(256), 0, st, X, ldx,
+                       (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks);
+  }
 }
 
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
@@ -190,11 +330,17 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
   const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
   if (NB * MT * p.splits != p.grid || N % (16 * kWaves * p.nf) || K % 32) return hipErrorInvalidValue;
   const dim3 grid(p.grid);
-#define WD_GEMM_CASE(NF, MF) \
-  if (p.nf == NF && p.mf == MF) launch_mf<NF, MF>(grid, st, X, ldx, Wp, C, M, N, K, NB, MT, p.splits, p.ks_per_split);
+  bool launched = false;
+#define WD_GEMM_CASE(NF, MF)                                                                  \
+  if (p.nf == NF && p.mf == MF) {                                                             \
+    launch_mf<NF, MF>(grid, st, X, ldx, Wp, C, M, N, K, NB, MT, p.splits, p.ks_per_split);   \
+    launched = true;                                                                          \
+  }
   WD_GEMM_CASE(1, 1) WD_GEMM_CASE(1, 2) WD_GEMM_CASE(1, 3) WD_GEMM_CASE(1, 4)
   WD_GEMM_CASE(2, 1) WD_GEMM_CASE(2, 2) WD_GEMM_CASE(2, 3) WD_GEMM_CASE(2, 4)
+  WD_GEMM_CASE(1, 8) WD_GEMM_CASE(2, 8)
 #undef WD_GEMM_CASE
+  if (!launched) return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -15,6 +15,7 @@ namespace wd {
 struct GemmPlan {
   int nf = 1;            // 16-row weight groups per wave
   int mf = 4;            // 16-row activation fragments per row tile
+  int ck = 8;            // 32-wide K steps per LDS activation chunk
   int splits = 1;        // K splits = number of partial outputs
   int ks_per_split = 0;  // 32-wide K steps per split
   int grid = 0;

@@ -21,25 +21,40 @@ if not torch.cuda.is_available():
 import paper_2601_20332_amd as wd  # noqa: E402
 
 
-@pytest.mark.parametrize("name", ["llada8b", "dream7b"])
-def test_first_phases_at_full_width(name):
+# (workload, steps to check, sequences the oracle replays)
+CASES = [
+    ("llada8b", 10, None),        # a whole phase (R = 8) and the next refresh
+    ("dream7b", 10, None),
+    ("llada8b_long", 10, None),   # c = 832, 66-82 online rows (many-row GEMM path)
+    ("llada8b_batch16", 10, (0, 5)),  # ragged prompts; 528-624 online rows per step
+]
+
+
+@pytest.mark.parametrize("name,n_steps,seqs", CASES, ids=[c[0] for c in CASES])
+def test_first_phases_at_full_width(name, n_steps, seqs):
     w = synth.WORKLOADS[name]
     shape = synth.with_layers(w.model, 2)
     t0 = time.time()
     log(f"[case] {name} at full width, 2 layers")
     W = synth.Weights(shape)
     m = gpu_model(W)
-    prompts = synth.prompts(shape, [w.prompt_len])
-    n_steps = w.window.refresh_every + 2     # a whole phase and the next refresh
+    prompts = synth.prompts(shape, synth.prompt_lengths(w))
     steps, _ = run_gpu(m, prompts, w.gen_len, w.window, max_steps=n_steps)
     m.free()
     log(f"[gpu] {len(steps)} steps in {time.time() - t0:.1f}s")
     om = OracleModel(W, cache_budget_bytes=40e9)
-    rep = check_sequence(om, prompts[0], w.gen_len, w.window, steps, 0, 1, max_steps=n_steps)
-    print(f"PARITY {name}-2L steps={rep.steps} max_rel_logit_err={rep.max_rel:.3e} "
-          f"adopted_sel={rep.select_adopted} adopted_tok={rep.token_adopted} "
-          f"({time.time() - t0:.1f}s)", flush=True)
-    assert rep.steps == n_steps
+    check = range(len(prompts)) if seqs is None else seqs
+    if seqs is not None:
+        # the shortest and the longest prompt of the batch
+        lens = [len(p) for p in prompts]
+        check = sorted({lens.index(min(lens)), lens.index(max(lens))})
+    for b in check:
+        rep = check_sequence(om, prompts[b], w.gen_len, w.window, steps, b, len(prompts),
+                             max_steps=n_steps)
+        print(f"PARITY {name}-2L seq={b} prompt={len(prompts[b])} steps={rep.steps} "
+              f"max_rel_logit_err={rep.max_rel:.3e} adopted_sel={rep.select_adopted} "
+              f"adopted_tok={rep.token_adopted} ({time.time() - t0:.1f}s)", flush=True)
+        assert rep.steps == n_steps
 
 
 def test_llada8b_32_layers_window_covering_everything_equals_full_path():
