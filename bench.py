@@ -151,6 +151,9 @@ def main():
     ap.add_argument("--no-full", action="store_true", help="skip the full-sequence comparison")
     ap.add_argument("--no-events", action="store_true",
                     help="time without the per-launch GEMM events (no roofline)")
+    ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
+                    help="only run 4 plain device-to-device copies of MIB MiB (the reference "
+                         "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -159,6 +162,15 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        a = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        b = torch.empty_like(a)
+        for _ in range(4):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_dispatch": n, "dispatches": 4}), flush=True)
+        return
     import synth
     import paper_2601_20332_amd as wd
 
