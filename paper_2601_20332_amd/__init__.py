@@ -62,6 +62,13 @@ class StepOut(ctypes.Structure):
 
 
 def _load() -> ctypes.CDLL:
+    # PyTorch ships its own HIP runtime (same soname as /opt/rocm's).  Loading
+    # torch first makes libwd bind to that one, so a process never holds two
+    # HIP/HSA runtimes, whatever order the caller imports things in.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2601_20332_amd.build` "
                           "(or __graft_entry__.build())")

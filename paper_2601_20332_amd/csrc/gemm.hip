@@ -285,9 +285,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
 // 16*MF rows; wide matrices (N >= 16384) stream best with 2 weight groups
 // per wave and as few K splits as give >= 384 workgroups, narrower ones with
 // 1 group per wave and >= 512 workgroups.  Above 64 rows (refresh steps, the
-// full-sequence path, batches): 128-row tiles and 2 weight groups per wave
-// (16 MFMAs per 16-byte weight load), software-pipelined, with K splits only
-// until 256 workgroups run (split-K partials cost rows*N*4 bytes each).
+// full-sequence path, batches): 128-row tiles, 2 weight groups per wave,
+// software-pipelined, K splits until 256 workgroups run (split-K partials
+// cost rows*N*4 bytes each).
 GemmPlan plan_gemm_bf16(int M, int N, int K) {
   GemmPlan p;
   const int KT = K / 32;
