@@ -12,8 +12,10 @@ denoising step (refresh and normal steps) until all 256 positions are
 decoded.  `value` is denoising steps per second over the timed generations.
 Also reported: decoded tokens/s, the speedup over standard full-sequence
 decoding on the same GPU and kernels, the roofline of the dominant kernel
-(the projection GEMM, timed with HIP events on the library's stream) and the
-CPU oracle on a bounded sample of the same workload.
+(the few-row projection GEMM of the normal steps, k_gemm_bf16, timed with HIP
+events on the library's stream; HBM bound), the same for the 128-row-tile GEMM
+of the refresh steps (k_gemm_bf16_big; MFMA bound) and the CPU oracle on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -42,16 +44,126 @@ def gemm_source_hash() -> str:
     return hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per GEMM launch from the committed rocprofv3 counter runs, if they
-    were taken on the current kernel source."""
+# GEMM kernel classes of wd_profile_read and the kernel each one is
+KERNEL_CLASSES = {1: "k_gemm_bf16", 2: "k_gemm_bf16_big"}
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of one GEMM kernel from the committed rocprofv3 counter
+    runs, if they were taken on the current kernel source."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
     if rec.get("gemm_source_sha256_16") != gemm_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
+
+
+def kernel_class_of(name: str):
+    """WD_PROF_* class of a kernel name as rocprofv3 prints it."""
+    if "k_gemm_bf16_big<" in name:
+        return 2
+    if "k_gemm_bf16<" in name:
+        return 1
+    return None
+
+
+def read_counter_csv(folder: str):
+    """(kernel name, counter value) rows of a rocprofv3 --pmc -f csv output folder."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        sys.exit(f"no counter_collection.csv under {folder}")
+    rows = []
+    for f in files:
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                rows.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def pmc_summary(gemm_fetch: str, gemm_write: str, copy_fetch: str, copy_write: str,
+                copy_mib: int):
+    """Turn the four rocprofv3 counter runs (FETCH_SIZE and WRITE_SIZE, in KiB per
+    dispatch, over one generation and over plain copies of copy_mib MiB) into HBM
+    bytes per launch of each GEMM kernel; writes TRAFFIC_FILE and prints a table."""
+    copy_bytes = copy_mib << 20
+
+    def copy_scale(folder):
+        vals = [v for n, v in read_counter_csv(folder) if "copyBuffer" in n]
+        if not vals:
+            sys.exit(f"no copy dispatch in {folder}")
+        return copy_bytes / (sum(vals) / len(vals))
+
+    sf, sw = copy_scale(copy_fetch), copy_scale(copy_write)
+    per = {}
+    for folder, key, scale in ((gemm_fetch, "fetch", sf), (gemm_write, "write", sw)):
+        for name, v in read_counter_csv(folder):
+            cls = kernel_class_of(name)
+            if cls is None:
+                continue
+            k = KERNEL_CLASSES[cls]
+            d = per.setdefault(k, {"fetch": [], "write": [], "instances": {}})
+            d[key].append(v * scale)
+            inst = name.split("(")[0].replace("void ", "")
+            di = d["instances"].setdefault(inst, {"fetch": [], "write": []})
+            di[key].append(v * scale)
+    kernels = {}
+    lines = ["| kernel instance | dispatches | fetched MB / dispatch | written MB / dispatch |",
+             "|---|---|---|---|"]
+    for k, d in per.items():
+        if len(d["fetch"]) != len(d["write"]):
+            sys.exit(f"{k}: {len(d['fetch'])} FETCH_SIZE vs {len(d['write'])} WRITE_SIZE dispatches")
+        n = len(d["fetch"])
+        f, w = sum(d["fetch"]) / n, sum(d["write"]) / n
+        kernels[k] = {"dispatches": n, "hbm_fetch_bytes_per_launch": round(f),
+                      "hbm_write_bytes_per_launch": round(w), "hbm_bytes_per_launch": round(f + w)}
+        for inst, di in sorted(d["instances"].items(), key=lambda x: -len(x[1]["fetch"])):
+            m = len(di["fetch"])
+            lines.append(f"| `{inst}` | {m} | {sum(di['fetch']) / m / 1e6:.1f} | "
+                         f"{sum(di['write']) / max(1, len(di['write'])) / 1e6:.2f} |")
+    rec = {"gemm_source_sha256_16": gemm_source_hash(), "copy_mib": copy_mib,
+           "fetch_bytes_per_count": round(sf, 4), "write_bytes_per_count": round(sw, 4),
+           "kernels": kernels}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec, indent=1))
+    print("\n".join(lines))
+
+
+def roofline_of(model, kernel_class: int, elapsed_ev: float):
+    """Roofline entry of one GEMM kernel from the event-timed launches of the
+    instrumented pass: the few-row kernel streams its weights (HBM bound), the
+    128-row-tile kernel is priced against dense bf16 MFMA."""
+    import paper_2601_20332_amd as wd
+    launches, ms, alg_bytes, alg_flops = wd.wd_profile_read(model, kernel_class)
+    if launches <= 0 or ms <= 0:
+        return None
+    name = KERNEL_CLASSES[kernel_class]
+    avg_s = ms / 1e3 / launches
+    gbs = alg_bytes / launches / avg_s / 1e9
+    tfs = alg_flops / launches / avg_s / 1e12
+    hbm = kernel_class == 1
+    achieved, peak = (gbs, HBM_PEAK_GBS) if hbm else (tfs, BF16_PEAK_TFLOPS)
+    return {
+        "kernel": name,
+        "bound": "hbm" if hbm else "mfma",
+        "achieved": round(achieved, 1),
+        "peak": peak,
+        "unit": "GB/s" if hbm else "TFLOP/s",
+        "frac": round(achieved / peak, 4),
+        "traffic": measured_traffic(name),
+        "launches": launches,
+        "avg_launch_us": round(avg_s * 1e6, 2),
+        "alg_bytes_per_launch": round(alg_bytes / launches),
+        "alg_flops_per_launch": round(alg_flops / launches),
+        "alg_gbs": round(gbs, 1),
+        "tflops": round(tfs, 1),
+        "share_of_step_time": round(ms / 1e3 / elapsed_ev, 3),
+    }
 
 
 def upload_model(shape, device):
@@ -154,7 +266,15 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
                     help="only run 4 plain device-to-device copies of MIB MiB (the reference "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("GEMM_FETCH", "GEMM_WRITE", "COPY_FETCH",
+                                                        "COPY_WRITE"),
+                    help="only turn four rocprofv3 --pmc csv folders into HBM bytes per GEMM "
+                         "launch (copies of --calibrate-copy MiB, default 1024), write "
+                         "profiles/gemm_bf16_traffic.json and exit; needs no GPU")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary, copy_mib=args.calibrate_copy or 1024)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the windowed step of one batch runs on one MI355X "
@@ -200,7 +320,7 @@ def main():
     # Roofline of the dominant kernel: the same generations again, now with a
     # HIP event pair around every projection-GEMM launch on the library's stream
     # (kept out of the pass above, whose clock gives `value`).
-    roofline = None
+    roofline = roofline_tiled = None
     if not args.no_events:
         wd.wd_profile_enable(model, True)
         torch.cuda.synchronize()
@@ -209,27 +329,13 @@ def main():
             generation(model, prompts, w.gen_len, wc, n_steps)
         torch.cuda.synchronize()
         elapsed_ev = time.perf_counter() - t_ev
-        launches, ms, alg_bytes, alg_flops = wd.wd_profile_read(model)
+        # the dominant kernel: few-row weight-streaming GEMM of the normal steps
+        roofline = roofline_of(model, wd.WD_PROF_GEMM_ROWS, elapsed_ev)
+        # second: the 128-row-tile GEMM of the refresh steps
+        roofline_tiled = roofline_of(model, wd.WD_PROF_GEMM_TILED, elapsed_ev)
         wd.wd_profile_enable(model, False)
-        if launches > 0 and ms > 0:
-            avg_s = ms / 1e3 / launches
-            achieved = alg_bytes / launches / avg_s / 1e9
-            roofline = {
-                "kernel": "k_gemm_bf16 (all projection and LM-head GEMM launches)",
-                "bound": "hbm",
-                "achieved": round(achieved, 1),
-                "peak": HBM_PEAK_GBS,
-                "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": measured_traffic(),
-                "launches": launches,
-                "avg_launch_us": round(avg_s * 1e6, 2),
-                "alg_bytes_per_launch": round(alg_bytes / launches),
-                "mfma_tflops": round(alg_flops / (ms / 1e3) / 1e12, 1),
-                "mfma_frac": round(alg_flops / (ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
-                "share_of_step_time": round(ms / 1e3 / elapsed_ev, 3),
-                "instrumented_pass_s": round(elapsed_ev, 3),
-            }
+        if roofline:
+            roofline["instrumented_pass_s"] = round(elapsed_ev, 3)
 
     full_speedup = None
     if not args.no_full:
@@ -281,6 +387,7 @@ def main():
         "decoded_tokens_per_s": round(args.steps * B * w.gen_len / elapsed, 3),
         "speedup_vs_full_sequence": full_speedup,
         "roofline": roofline,
+        "roofline_tiled_gemm": roofline_tiled,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -211,21 +211,33 @@ void wd_free_seq(wd_seq* s); /* NULL is a no-op; synchronizes the stream */
 
 /* ---- kernel timing ------------------------------------------------------------- */
 
-/* When enabled, every launch of the projection GEMM kernel (Q/K/V, output,
- * gate/up, down and LM-head products) on this model's stream is bracketed by
- * a pair of HIP events, and the launch's algorithmic traffic and work are
- * recorded: bytes = weights (N*K elements) + input rows (M*K elements) +
- * fp32 output (M*N*4), flops = 2*M*N*K.  Up to 1 << 20 launches are kept
- * between reads (WD_ERR_OUT_OF_MEMORY from the launching call beyond that).
- * Disabled by default; enabling or disabling discards unread records. */
+/* Kernel classes of the recorded GEMM launches. */
+enum {
+  WD_PROF_ALL = 0,        /* every recorded launch */
+  WD_PROF_GEMM_ROWS = 1,  /* k_gemm_bf16: at most 64 rows, each weight read once (normal
+                             steps, LM head) */
+  WD_PROF_GEMM_TILED = 2, /* k_gemm_bf16_big: more than 64 rows in 128-row tiles (refresh
+                             and full-sequence steps) */
+  WD_PROF_GEMM_F32 = 3    /* k_gemm_f32: fp32 models */
+};
+
+/* When enabled, every launch of the projection GEMM kernels (Q/K/V, output,
+ * gate/up, down and LM-head products) on this model's stream records a pair
+ * of HIP events from its own dispatch (start and end of the kernel), and the
+ * launch's kernel class and algorithmic traffic and work are recorded: bytes = weights (N*K elements) + input rows (M*K
+ * elements) + fp32 output (M*N*4), flops = 2*M*N*K.  Up to 1 << 20 launches
+ * are kept (WD_ERR_OUT_OF_MEMORY from the launching call beyond that).
+ * Disabled by default; every call discards the records taken so far. */
 wd_status wd_profile_enable(wd_model* m, int32_t enable);
 
-/* Synchronizes the model's stream, then returns the launches recorded since
- * the last read, the sum of their event-measured durations (milliseconds) and
- * of their algorithmic bytes and flops, and clears the records.  Any output
- * pointer may be NULL. */
-wd_status wd_profile_read(wd_model* m, int64_t* launches, double* total_ms, double* alg_bytes,
-                          double* alg_flops);
+/* Synchronizes the model's stream, then returns, over the launches of class
+ * `kernel` (WD_PROF_*) recorded since profiling was last enabled, their
+ * number, the sum of their event-measured durations (milliseconds) and of
+ * their algorithmic bytes and flops.  Records are kept, so several classes
+ * can be read.  Any output pointer may be NULL; an unknown class is
+ * WD_ERR_INVALID_ARG. */
+wd_status wd_profile_read(wd_model* m, int32_t kernel, int64_t* launches, double* total_ms,
+                          double* alg_bytes, double* alg_flops);
 
 /* ---- host-only helpers -------------------------------------------------------- */
 

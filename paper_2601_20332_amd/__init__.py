@@ -99,7 +99,7 @@ def _load() -> ctypes.CDLL:
         "wd_plan": (i32, [i32, i32, ctypes.POINTER(WindowConfig), i32, pi32, pi32, pi32, pi32, pi32]),
         "wd_last_error": (ctypes.c_char_p, []),
         "wd_profile_enable": (i32, [P, i32]),
-        "wd_profile_read": (i32, [P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
+        "wd_profile_read": (i32, [P, i32, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
@@ -330,11 +330,16 @@ def wd_profile_enable(model: Model, enable: bool = True) -> None:
     _check(lib.wd_profile_enable(model.handle, int(bool(enable))))
 
 
-def wd_profile_read(model: Model):
-    """(launches, total_ms, algorithmic bytes, algorithmic flops) since the last read."""
+# kernel classes of wd_profile_read
+WD_PROF_ALL, WD_PROF_GEMM_ROWS, WD_PROF_GEMM_TILED, WD_PROF_GEMM_F32 = 0, 1, 2, 3
+
+
+def wd_profile_read(model: Model, kernel: int = WD_PROF_ALL):
+    """(launches, total_ms, algorithmic bytes, algorithmic flops) of the GEMM
+    launches of one kernel class recorded since profiling was enabled."""
     n, ms, by, fl = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
-    _check(lib.wd_profile_read(model.handle, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(by),
-                               ctypes.byref(fl)))
+    _check(lib.wd_profile_read(model.handle, int(kernel), ctypes.byref(n), ctypes.byref(ms),
+                               ctypes.byref(by), ctypes.byref(fl)))
     return n.value, ms.value, by.value, fl.value
 
 

@@ -181,6 +181,7 @@ struct wd_model {
   std::vector<hipEvent_t> ev;    // event pool, two per recorded launch
   size_t n_rec = 0;              // launches recorded since the last read
   std::vector<double> rec_bytes, rec_flops;
+  std::vector<int> rec_kind;     // WD_PROF_* class of each recorded launch
 };
 
 namespace {
@@ -367,28 +368,31 @@ wd_status wd_profile_enable(wd_model* m, int32_t enable) {
   m->n_rec = 0;
   m->rec_bytes.clear();
   m->rec_flops.clear();
+  m->rec_kind.clear();
   return WD_OK;
 }
 
-wd_status wd_profile_read(wd_model* m, int64_t* launches, double* total_ms, double* alg_bytes,
-                          double* alg_flops) {
+wd_status wd_profile_read(wd_model* m, int32_t kernel, int64_t* launches, double* total_ms,
+                          double* alg_bytes, double* alg_flops) {
   if (!m) return fail(WD_ERR_INVALID_ARG, "model is NULL");
+  if (kernel < WD_PROF_ALL || kernel > WD_PROF_GEMM_F32)
+    return fail(WD_ERR_INVALID_ARG, "unknown kernel class %d", kernel);
   WD_HIP(hipStreamSynchronize(m->stream));
+  int64_t n = 0;
   double ms = 0.0, by = 0.0, fl = 0.0;
   for (size_t i = 0; i < m->n_rec; ++i) {
+    if (kernel != WD_PROF_ALL && m->rec_kind[i] != kernel) continue;
     float t = 0.f;
     WD_HIP(hipEventElapsedTime(&t, m->ev[2 * i], m->ev[2 * i + 1]));
+    ++n;
     ms += t;
     by += m->rec_bytes[i];
     fl += m->rec_flops[i];
   }
-  if (launches) *launches = (int64_t)m->n_rec;
+  if (launches) *launches = n;
   if (total_ms) *total_ms = ms;
   if (alg_bytes) *alg_bytes = by;
   if (alg_flops) *alg_flops = fl;
-  m->n_rec = 0;
-  m->rec_bytes.clear();
-  m->rec_flops.clear();
   return WD_OK;
 }
 
@@ -556,8 +560,10 @@ struct Rows {
   WdStepGeom g;
 };
 
-// Event pair around one GEMM launch when kernel timing is on.
-wd_status profile_begin(wd_model& m) {
+// Event pair for one GEMM launch when kernel timing is on (null otherwise);
+// the launch records both events from its own dispatch.
+wd_status profile_begin(wd_model& m, hipEvent_t* e0, hipEvent_t* e1) {
+  *e0 = *e1 = nullptr;
   if (!m.profile) return WD_OK;
   if (m.n_rec >= (1u << 20)) return fail(WD_ERR_OUT_OF_MEMORY, "too many unread timing records");
   while (m.ev.size() < 2 * (m.n_rec + 1)) {
@@ -565,22 +571,23 @@ wd_status profile_begin(wd_model& m) {
     WD_HIP(hipEventCreate(&e));
     m.ev.push_back(e);
   }
-  WD_HIP(hipEventRecord(m.ev[2 * m.n_rec], m.stream));
+  *e0 = m.ev[2 * m.n_rec];
+  *e1 = m.ev[2 * m.n_rec + 1];
   return WD_OK;
 }
 
-wd_status profile_end(wd_model& m, int M, int N, int K, size_t esz) {
+wd_status profile_end(wd_model& m, int kind, int M, int N, int K, size_t esz) {
   if (!m.profile) return WD_OK;
-  WD_HIP(hipEventRecord(m.ev[2 * m.n_rec + 1], m.stream));
   m.rec_bytes.push_back((double)N * K * esz + (double)M * K * esz + (double)M * N * 4);
   m.rec_flops.push_back(2.0 * M * N * K);
+  m.rec_kind.push_back(kind);
   m.n_rec++;
   return WD_OK;
 }
 
 template <typename T>
 wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
-                      int max_splits, int* splits) {
+                      int max_splits, int* splits, int* kind, hipEvent_t e0, hipEvent_t e1) {
   const wd_model& m = *s->m;
   if (m.cfg.dtype == WD_DTYPE_BF16) {
     wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K);
@@ -591,11 +598,13 @@ wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, float* C, i
     }
     if ((size_t)p.splits * M * N > s->C_floats && C == s->C)
       return fail(WD_ERR_DEVICE, "internal: partial buffer too small");
-    WD_HIP(wd::gemm_bf16((const uint16_t*)X, ldx, W, C, M, N, K, p, m.stream));
+    WD_HIP(wd::gemm_bf16((const uint16_t*)X, ldx, W, C, M, N, K, p, m.stream, e0, e1));
     *splits = p.splits;
+    *kind = p.mf == 8 ? WD_PROF_GEMM_TILED : WD_PROF_GEMM_ROWS;
   } else {
-    WD_HIP(wd::gemm_f32((const float*)X, ldx, (const float*)W, C, M, N, K, m.stream));
+    WD_HIP(wd::gemm_f32((const float*)X, ldx, (const float*)W, C, M, N, K, m.stream, e0, e1));
     *splits = 1;
+    *kind = WD_PROF_GEMM_F32;
   }
   return WD_OK;
 }
@@ -604,9 +613,11 @@ template <typename T>
 wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
                int max_splits, int* splits) {
   wd_model& m = *s->m;
-  WD_TRY(profile_begin(m));
-  WD_TRY(gemm_launch<T>(s, X, ldx, W, C, M, N, K, max_splits, splits));
-  return profile_end(m, M, N, K, m.esz);
+  int kind = WD_PROF_ALL;
+  hipEvent_t e0, e1;
+  WD_TRY(profile_begin(m, &e0, &e1));
+  WD_TRY(gemm_launch<T>(s, X, ldx, W, C, M, N, K, max_splits, splits, &kind, e0, e1));
+  return profile_end(m, kind, M, N, K, m.esz);
 }
 
 template <typename T>

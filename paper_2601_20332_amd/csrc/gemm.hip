@@ -10,6 +10,8 @@
 // At the row counts of a normal step (tens of rows) the kernel is bound by
 // HBM bandwidth on the weight stream; the split-K factor is chosen so that a
 // launch has enough workgroups to keep every CU's memory pipeline full.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -311,20 +313,32 @@ GemmPlan plan_gemm_bf16(int M, int N, int K) {
   return p;
 }
 
+// With a start/stop event pair, the launch records them from its own dispatch
+// (the kernel's execution time, as a kernel trace reports it).
+template <typename F, typename... A>
+static void launch_timed(F kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                         A... args) {
+  if (e0)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, args...);
+}
+
 template <int NF, int MF>
-static void launch_mf(dim3 grid, hipStream_t st, const uint16_t* X, int ldx, const void* Wp,
-                      float* C, int M, int N, int K, int NB, int MT, int S, int ks) {
+static void launch_mf(dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, const uint16_t* X,
+                      int ldx, const void* Wp, float* C, int M, int N, int K, int NB, int MT,
+                      int S, int ks) {
   if constexpr (MF == 8) {
-    hipLaunchKernelGGL((k_gemm_bf16_big<NF>), grid, dim3(256), 0, st, X, ldx, (const u32x4*)Wp, C,
-                       M, N, K, NB, MT, S, ks);
+    launch_timed(k_gemm_bf16_big<NF>, grid, st, e0, e1, X, ldx, (const u32x4*)Wp, C, M, N, K, NB,
+                 MT, S, ks);
   } else {
-    hipLaunchKernelGGL((k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4, 8>), grid, dim3(256), 0, st, X, ldx,
-                       (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks);
+    launch_timed(k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4, 8>, grid, st, e0, e1, X, ldx,
+                 (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks);
   }
 }
 
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
-                     const GemmPlan& p, hipStream_t st) {
+                     const GemmPlan& p, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (M <= 0) return hipSuccess;
   const int NB = N / (16 * kWaves * p.nf);
   const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
@@ -333,7 +347,8 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
   bool launched = false;
 #define WD_GEMM_CASE(NF, MF)                                                                  \
   if (p.nf == NF && p.mf == MF) {                                                             \
-    launch_mf<NF, MF>(grid, st, X, ldx, Wp, C, M, N, K, NB, MT, p.splits, p.ks_per_split);   \
+    launch_mf<NF, MF>(grid, st, ev_start, ev_stop, X, ldx, Wp, C, M, N, K, NB, MT, p.splits, \
+                      p.ks_per_split);                                                        \
     launched = true;                                                                          \
   }
   WD_GEMM_CASE(1, 1) WD_GEMM_CASE(1, 2) WD_GEMM_CASE(1, 3) WD_GEMM_CASE(1, 4)
@@ -386,10 +401,10 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
 }
 
 hipError_t gemm_f32(const float* X, int ldx, const float* W, float* C, int M, int N, int K,
-                    hipStream_t st) {
+                    hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (M <= 0) return hipSuccess;
   dim3 grid(N / 64, (M + 63) / 64);
-  hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, X, ldx, W, C, M, N, K);
+  launch_timed(k_gemm_f32, grid, st, ev_start, ev_stop, X, ldx, W, C, M, N, K);
   return hipGetLastError();
 }
 

@@ -22,10 +22,12 @@ struct GemmPlan {
 };
 GemmPlan plan_gemm_bf16(int M, int N, int K);
 hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st);
+// ev_start / ev_stop (optional, both or neither): recorded by the launch itself
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
-                     const GemmPlan& p, hipStream_t st);
+                     const GemmPlan& p, hipStream_t st, hipEvent_t ev_start = nullptr,
+                     hipEvent_t ev_stop = nullptr);
 hipError_t gemm_f32(const float* X, int ldx, const float* W, float* C, int M, int N, int K,
-                    hipStream_t st);
+                    hipStream_t st, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // ---- row-wise layer pieces (layer.hip) -------------------------------------------------
 // h[r] = emb[x[row_tok[r]]]; a[r] = RMSNorm(h[r]) * gamma

@@ -74,8 +74,7 @@ __global__ __launch_bounds__(1024) void k_residual_norm(float* __restrict__ h,
   for (int it = 0; it < 4; ++it) {
     const int i = (threadIdx.x + it * 1024) * 4;
     if (i < H) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < S; ++s) acc += *(const f32x4*)(C + ((long)s * M + r) * H + i);
+      const f32x4 acc = split_sum((const f32x4*)(C + r * H + i), (long)M * H / 4, S);
       v[it] = *(const f32x4*)(hr + i) + acc;
       *(f32x4*)(hr + i) = v[it];
       ss += v[it][0] * v[it][0] + v[it][1] * v[it][1] + v[it][2] * v[it][2] + v[it][3] * v[it][3];
@@ -116,12 +115,8 @@ __global__ void k_qkv_epilogue(const float* __restrict__ C, int S, int M, int N,
                                long cache_rows) {
   const int r = blockIdx.x, hs = blockIdx.y, i = threadIdx.x, half = d >> 1;
   const int col = hs * d + i;
-  float x0 = 0.f, x1 = 0.f;
-  for (int s = 0; s < S; ++s) {
-    const float* cr = C + ((long)s * M + r) * N;
-    x0 += cr[col];
-    x1 += cr[col + half];
-  }
+  float x0, x1;
+  split_sum2(C + (long)r * N + col, C + (long)r * N + col + half, (long)M * N, S, x0, x1);
   if (bias) {
     x0 += Elem<T>::load(bias + col);
     x1 += Elem<T>::load(bias + col + half);
@@ -159,27 +154,27 @@ hipError_t qkv_epilogue(const float* C, int S, int M, const T* bias, const float
 }
 
 // ---- SwiGLU -----------------------------------------------------------------------------
+// Four consecutive features per thread; F is a multiple of 4.
 template <typename T>
 __global__ void k_swiglu(const float* __restrict__ C, int S, int M, int F, T* __restrict__ out) {
-  const long total = (long)M * F;
+  const long total = (long)M * F / 4;
   for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < total;
        e += (long)gridDim.x * blockDim.x) {
-    const long r = e / F;
-    const int f = (int)(e - r * F);
-    float g = 0.f, u = 0.f;
-    for (int s = 0; s < S; ++s) {
-      const float* cr = C + ((long)s * M + r) * (2L * F);
-      g += cr[f];
-      u += cr[F + f];
-    }
-    out[e] = Elem<T>::from_f(g / (1.0f + expf(-g)) * u);
+    const long r = e / (F / 4);
+    const int f = (int)(e - r * (F / 4)) * 4;
+    const float* cr = C + r * (2L * F) + f;
+    f32x4 g, u;
+    split_sum2((const f32x4*)cr, (const f32x4*)(cr + F), (long)M * F / 2, S, g, u);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) out[r * F + f + q] = Elem<T>::from_f(g[q] / (1.0f + expf(-g[q])) * u[q]);
   }
 }
 
 template <typename T>
 hipError_t swiglu(const float* C, int S, int M, int F, T* out, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  const long total = (long)M * F;
+  if (F % 4) return hipErrorInvalidValue;
+  const long total = (long)M * F / 4;
   const int blocks = (int)std::min<long>((total + 255) / 256, 8192);
   hipLaunchKernelGGL(k_swiglu<T>, dim3(blocks), dim3(256), 0, st, C, S, M, F, out);
   return hipGetLastError();
@@ -241,6 +236,7 @@ constexpr int kAttD = 128;
 constexpr int kKT = 64;              // keys per tile
 constexpr int kKPitch = kAttD + 8;   // bf16 elements per K row in LDS
 constexpr int kVPitch = kKT + 8;     // bf16 elements per V^T row in LDS
+constexpr int kMaxSplit = 16;        // most key splits of one attention launch
 
 // Split-KV: blockIdx.z = query block * nsplit + split; split s covers keys
 // [s * keys_per_split, (s + 1) * keys_per_split) of [0, c).  With nsplit == 1
@@ -287,24 +283,38 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
   float m_run = -INFINITY, l_run = 0.f;
   const float scale = 0.08838834764831845f;  // 1/sqrt(128)
 
+  // K/V tile of 64 keys x 256 B each: thread tid covers keys (tid >> 4) + 16 i,
+  // 16-byte chunk tid & 15.  The next tile's loads are issued before the
+  // current tile is computed; addresses are clamped to the last key and the
+  // keys past c are zeroed when the tile is stored.
+  const int tkey = tid >> 4, tch = tid & 15;
+  u32x4 kr[4], vr[4];
+  auto load_tile = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const long kk = min(j0 + tkey + 16 * i, c - 1);
+      kr[i] = *(const u32x4*)(kb + kk * kAttD + tch * 8);
+      vr[i] = *(const u32x4*)(vb + kk * kAttD + tch * 8);
+    }
+  };
+  if (key_lo < c) load_tile(key_lo);
   for (int j0 = key_lo; j0 < c; j0 += kKT) {
     __syncthreads();
-    // K tile: 64 rows x 256 B; V tile transposed into Vt[dd][key]
-    for (int e = tid; e < kKT * 16; e += 256) {
-      const int key = e >> 4, ch = e & 15;
-      u32x4 kv = zero4, vv = zero4;
-      if (j0 + key < c) {
-        kv = *(const u32x4*)(kb + (long)(j0 + key) * kAttD + ch * 8);
-        vv = *(const u32x4*)(vb + (long)(j0 + key) * kAttD + ch * 8);
-      }
-      *(u32x4*)(Ks + key * kKPitch + ch * 8) = kv;
+    // K rows as they are; V transposed into Vt[dd][key]
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        Vt[(ch * 8 + 2 * i) * kVPitch + key] = (uint16_t)(vv[i] & 0xffffu);
-        Vt[(ch * 8 + 2 * i + 1) * kVPitch + key] = (uint16_t)(vv[i] >> 16);
+    for (int i = 0; i < 4; ++i) {
+      const int key = tkey + 16 * i;
+      const bool ok = j0 + key < c;
+      const u32x4 kv = ok ? kr[i] : zero4, vv = ok ? vr[i] : zero4;
+      *(u32x4*)(Ks + key * kKPitch + tch * 8) = kv;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        Vt[(tch * 8 + 2 * w) * kVPitch + key] = (uint16_t)(vv[w] & 0xffffu);
+        Vt[(tch * 8 + 2 * w + 1) * kVPitch + key] = (uint16_t)(vv[w] >> 16);
       }
     }
     __syncthreads();
+    load_tile(min(j0 + kKT, c - 1));
     if (!wave_active) continue;
 
     // S^T[key][query] for 4 subtiles of 16 keys
@@ -401,15 +411,27 @@ __global__ __launch_bounds__(128) void k_attn_combine(const float* __restrict__ 
                                                       const float* __restrict__ ml, int nsplit,
                                                       int M, int nh, uint16_t* __restrict__ o) {
   const int r = blockIdx.x, h = blockIdx.y, dd = threadIdx.x;
-  float mx = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, ml[(((long)s * M + r) * nh + h) * 2]);
-  float l = 0.f, acc = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const long pr = ((long)s * M + r) * nh + h;
-    const float w = expf(ml[pr * 2] - mx);
-    l += w * ml[pr * 2 + 1];
-    acc += w * part[pr * kAttD + dd];
+  // every split's (m, l, O) in flight at once; nsplit <= kMaxSplit
+  float ms[kMaxSplit], ls[kMaxSplit], os[kMaxSplit];
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s) {
+    const long pr = ((long)min(s, nsplit - 1) * M + r) * nh + h;
+    ms[s] = ml[pr * 2];
+    ls[s] = ml[pr * 2 + 1];
+    os[s] = part[pr * kAttD + dd];
   }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s)
+    if (s < nsplit) mx = fmaxf(mx, ms[s]);
+  float l = 0.f, acc = 0.f;
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s)
+    if (s < nsplit) {
+      const float w = expf(ms[s] - mx);
+      l += w * ls[s];
+      acc += w * os[s];
+    }
   o[((long)r * nh + h) * kAttD + dd] = f2bf(acc / l);
 }
 
@@ -429,7 +451,7 @@ hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint1
   // split the keys until about 512 workgroups run, if the partial buffer allows
   const int tiles = (cmax + kKT - 1) / kKT;
   int nsplit = std::min<long>(tiles, std::max<long>(1, (512 + n_heads * qblocks - 1) / (n_heads * qblocks)));
-  nsplit = std::min(nsplit, 16);
+  nsplit = std::min(nsplit, kMaxSplit);
   while (nsplit > 1 && (long)nsplit * M * n_heads * (kAttD + 2) > part_floats) --nsplit;
   const int tps = (tiles + nsplit - 1) / nsplit;
   nsplit = (tiles + tps - 1) / tps;

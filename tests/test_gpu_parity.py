@@ -183,3 +183,35 @@ def test_deterministic_runs():
     for b in range(2):
         np.testing.assert_array_equal(f1[0][b], f2[0][b])
     m.free()
+
+
+def test_profile_records_by_kernel_class():
+    """Timing records: every GEMM launch lands in exactly one kernel class, the
+    many-row refresh products in the 128-row-tile kernel and the few-row normal
+    steps in the weight-streaming kernel; algorithmic bytes follow the stated
+    formula; an unknown class is rejected."""
+    shape = MICRO_GQA
+    W = synth.Weights(shape, seed=4)
+    m = gpu_model(W)
+    prompts = synth.prompts(shape, [60, 70])          # refresh rows > 64, normal rows <= 64
+    win = synth.WindowSettings(6, 10, 4, 2)
+    wd.wd_profile_enable(m, True)
+    run_gpu(m, prompts, 16, win, max_steps=4, keep_logits=False)   # steps 0-3: one refresh
+    n_all, ms_all, by_all, fl_all = wd.wd_profile_read(m, wd.WD_PROF_ALL)
+    n_rows, ms_rows, by_rows, _ = wd.wd_profile_read(m, wd.WD_PROF_GEMM_ROWS)
+    n_tiled, ms_tiled, by_tiled, _ = wd.wd_profile_read(m, wd.WD_PROF_GEMM_TILED)
+    n_f32 = wd.wd_profile_read(m, wd.WD_PROF_GEMM_F32)[0]
+    assert n_rows > 0 and n_tiled > 0 and n_f32 == 0
+    assert n_all == n_rows + n_tiled
+    assert ms_all > 0 and abs(ms_all - ms_rows - ms_tiled) <= 1e-6 * ms_all
+    assert abs(by_all - by_rows - by_tiled) <= 1e-9 * by_all
+    # one refresh step: 4 projections per layer through the tiled kernel
+    assert n_tiled == 4 * shape.n_layers
+    # reading does not consume the records; enabling again discards them
+    assert wd.wd_profile_read(m, wd.WD_PROF_ALL)[0] == n_all
+    wd.wd_profile_enable(m, True)
+    assert wd.wd_profile_read(m, wd.WD_PROF_ALL)[0] == 0
+    with pytest.raises(wd.WdError):
+        wd.wd_profile_read(m, 7)
+    wd.wd_profile_enable(m, False)
+    m.free()
