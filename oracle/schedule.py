@@ -31,6 +31,21 @@ Window-Diffusion (Sec. 4.2, Sec. 4.3):
   decoded inside the phase stay online until the next refresh
   (Sec. 4.3, and the refresh-cycle ablation of Sec. 5.3).
 
+Adaptive termination (Sec. 4.2, adaptive termination; optional, eos_id):
+
+* Once an <eos> token is decoded at a generated position e, the sequence
+  ends at e: end = e + 1 (the first such position if there are several;
+  end = S while none is decoded).  Positions at or after end are far-field
+  for good: they leave the active set, the online rows and the attention
+  context at once (the internal window stops advancing), and no later
+  window reaches them.
+* At a phase start W_ex and c are taken over [0, end) only: W_ex = the
+  first E undecoded positions below end, c = (E-th of them) + 1, or end
+  when fewer remain.  Within a phase the attention context is [0, min(c,
+  end)).
+* The sequence is finished when every position below end is decoded.  The
+  positions after it keep the mask token.
+
 Readings where the paper is silent:
 
 * A refresh happens at step 0 and then every R steps; a phase also ends
@@ -38,6 +53,8 @@ Readings where the paper is silent:
   positions remain (the next step then starts a new phase).
 * The refresh step is itself a decoding step (logits on A at every step).
 * Positions are absolute indices; batched sequences are independent.
+* Only generated positions end a sequence: an <eos> id inside the prompt
+  does not.
 """
 from __future__ import annotations
 
@@ -55,11 +72,11 @@ from .sampler import confidence, select_updates
 class StepRecord:
     t: int
     refresh: bool
-    ctx_len: int                 # c: the retained prefix [0, c)
+    ctx_len: int                 # attended prefix [0, c) (min(c, end) with <eos>)
     window: List[int]            # W_ex of the current phase
     active: List[int]            # A(t)
     online: List[int]            # rows computed this step (= [0, c) on a refresh)
-    phase_decoded: List[int]     # D_p(t) before this step's update
+    phase_decoded: List[int]     # D_p(t) below end, before this step's update
     logits: Optional[np.ndarray]  # [|A|, V] (None unless kept)
     tokens: np.ndarray           # argmax candidate per active row
     conf: np.ndarray             # float32 confidence per active row
@@ -78,19 +95,38 @@ def _apply_override(rec: StepRecord, override: Optional[Override]) -> None:
         rec.selected, rec.chosen_tokens = list(res[0]), dict(res[1])
 
 
-class WindowedDecoder:
+class _EosEnd:
+    """The live end of a sequence under adaptive termination: one past the
+    first generated position holding the <eos> token (S while there is none)."""
+
+    eos_id: Optional[int]
+    n_p: int
+    end: int
+    x: np.ndarray
+
+    def _apply_eos(self, positions) -> None:
+        if self.eos_id is None:
+            return
+        for p in positions:
+            if p >= self.n_p and int(self.x[p]) == self.eos_id:
+                self.end = min(self.end, int(p) + 1)
+
+
+class WindowedDecoder(_EosEnd):
     """Window-Diffusion decoding of one sequence with the oracle model."""
 
     def __init__(self, model: OracleModel, prompt: Sequence[int], gen_len: int,
-                 win: synth.WindowSettings):
+                 win: synth.WindowSettings, eos_id: Optional[int] = None):
         if win.n_active < 1 or win.unmask_per_step < 1 or win.refresh_every < 1:
             raise ValueError("window settings must be positive")
         if win.n_buffer < 0 or gen_len < 1:
             raise ValueError("bad window or generation length")
         self.model = model
         self.win = win
+        self.eos_id = eos_id
         self.n_p = len(prompt)
         self.S = self.n_p + gen_len
+        self.end = self.S                   # live positions are [0, end)
         mask = model.shape.mask_id
         self.x = np.concatenate([np.asarray(prompt, dtype=np.int64),
                                  np.full(gen_len, mask, dtype=np.int64)])
@@ -105,33 +141,40 @@ class WindowedDecoder:
 
     # -- bookkeeping -----------------------------------------------------
     def done(self) -> bool:
-        return bool(self.decoded.all())
+        return bool(self.decoded[:self.end].all())
 
     def needs_phase(self) -> bool:
         if self.j is None or self.j >= self.win.refresh_every:
             return True
-        return not any(not self.decoded[i] for i in self.window)
+        return not any(not self.decoded[i] and i < self.end for i in self.window)
 
     def slide(self) -> None:
         """Phase start: re-determine W_ex and the retained prefix [0, c)."""
-        und = np.flatnonzero(~self.decoded)
+        und = np.flatnonzero(~self.decoded[:self.end])
         E = self.win.external
         self.window = [int(i) for i in und[:E]]
-        self.ctx_len = int(und[E - 1]) + 1 if len(und) >= E else self.S
+        self.ctx_len = int(und[E - 1]) + 1 if len(und) >= E else self.end
         self.phase_decoded = []
         self.j = 0
 
+    def context(self) -> int:
+        """Length of the attended prefix this step."""
+        return min(self.ctx_len, self.end)
+
+    def live_phase_decoded(self) -> List[int]:
+        return [p for p in self.phase_decoded if p < self.end]
+
     def active(self) -> List[int]:
-        und = [i for i in self.window if not self.decoded[i]]
+        und = [i for i in self.window if not self.decoded[i] and i < self.end]
         return und[:self.win.n_active]
 
     def online(self) -> List[int]:
-        return sorted(set(self.active()) | set(self.phase_decoded))
+        return sorted(set(self.active()) | set(self.live_phase_decoded()))
 
     def buffer(self) -> List[int]:
         a = set(self.active())
         d = set(self.phase_decoded)
-        return [i for i in self.window if i not in a and i not in d]
+        return [i for i in self.window if i not in a and i not in d and i < self.end]
 
     # -- one diffusion step ------------------------------------------------
     def step(self, override: Optional[Override] = None, keep_logits: bool = False) -> StepRecord:
@@ -152,15 +195,15 @@ class WindowedDecoder:
         else:
             A = self.active()
             rows = self.online()
-            hO = m.forward_rows(self.x[rows], rows, self.cache, self.ctx_len)
+            hO = m.forward_rows(self.x[rows], rows, self.cache, self.context())
             where = {p: i for i, p in enumerate(rows)}
             hA = hO[[where[p] for p in A]]
         logits = m.logits(hA)
         tok, conf = confidence(logits, m.shape.mask_id)
         sel = select_updates(A, conf, self.win.unmask_per_step)
-        rec = StepRecord(t=self.t, refresh=refresh, ctx_len=self.ctx_len,
+        rec = StepRecord(t=self.t, refresh=refresh, ctx_len=self.context(),
                          window=list(self.window), active=list(A), online=rows,
-                         phase_decoded=list(self.phase_decoded),
+                         phase_decoded=self.live_phase_decoded(),
                          logits=logits, tokens=tok, conf=conf, selected=sel,
                          chosen_tokens={p: int(tok[A.index(p)]) for p in sel})
         _apply_override(rec, override)
@@ -169,6 +212,7 @@ class WindowedDecoder:
             self.x[p] = rec.chosen_tokens[p]
             self.decoded[p] = True
             self.phase_decoded.append(p)
+        self._apply_eos(rec.selected)
         self.t += 1
         self.j += 1
         if not keep_logits:
@@ -176,15 +220,20 @@ class WindowedDecoder:
         return rec
 
 
-class FullDecoder:
+class FullDecoder(_EosEnd):
     """Standard mask-based DLM decoding (Sec. 3.1): every step is a full forward
-    over all S positions; every undecoded position is a candidate."""
+    over all S positions; every undecoded position is a candidate.  With
+    eos_id, the forward and the candidates stop at the live end (the
+    adaptive-length counterpart of the windowed decoder)."""
 
-    def __init__(self, model: OracleModel, prompt: Sequence[int], gen_len: int, k: int):
+    def __init__(self, model: OracleModel, prompt: Sequence[int], gen_len: int, k: int,
+                 eos_id: Optional[int] = None):
         self.model = model
         self.k = k
+        self.eos_id = eos_id
         self.n_p = len(prompt)
         self.S = self.n_p + gen_len
+        self.end = self.S
         self.x = np.concatenate([np.asarray(prompt, dtype=np.int64),
                                  np.full(gen_len, model.shape.mask_id, dtype=np.int64)])
         self.decoded = np.zeros(self.S, dtype=bool)
@@ -192,39 +241,42 @@ class FullDecoder:
         self.t = 0
 
     def done(self) -> bool:
-        return bool(self.decoded.all())
+        return bool(self.decoded[:self.end].all())
 
     def step(self, override: Optional[Override] = None, keep_logits: bool = False) -> StepRecord:
         m = self.model
-        h, _, _ = m.forward(self.x)
-        cand = [int(i) for i in np.flatnonzero(~self.decoded)]
+        n = self.end
+        h, _, _ = m.forward(self.x[:n])
+        cand = [int(i) for i in np.flatnonzero(~self.decoded[:n])]
         logits = m.logits(h[cand])
         tok, conf = confidence(logits, m.shape.mask_id)
         sel = select_updates(cand, conf, self.k)
-        rec = StepRecord(t=self.t, refresh=True, ctx_len=self.S, window=cand, active=cand,
-                         online=list(range(self.S)), phase_decoded=[], logits=logits,
+        rec = StepRecord(t=self.t, refresh=True, ctx_len=n, window=cand, active=cand,
+                         online=list(range(n)), phase_decoded=[], logits=logits,
                          tokens=tok, conf=conf, selected=sel,
                          chosen_tokens={p: int(tok[cand.index(p)]) for p in sel})
         _apply_override(rec, override)
         for p in rec.selected:
             self.x[p] = rec.chosen_tokens[p]
             self.decoded[p] = True
+        self._apply_eos(rec.selected)
         self.t += 1
         if not keep_logits:
             rec.logits = None
         return rec
 
 
-def generate_windowed(model, prompt, gen_len, win, override=None, keep_logits=False):
-    dec = WindowedDecoder(model, prompt, gen_len, win)
+def generate_windowed(model, prompt, gen_len, win, override=None, keep_logits=False,
+                      eos_id=None):
+    dec = WindowedDecoder(model, prompt, gen_len, win, eos_id=eos_id)
     recs = []
     while not dec.done():
         recs.append(dec.step(override, keep_logits))
     return dec.x.copy(), recs
 
 
-def generate_full(model, prompt, gen_len, k, override=None, keep_logits=False):
-    dec = FullDecoder(model, prompt, gen_len, k)
+def generate_full(model, prompt, gen_len, k, override=None, keep_logits=False, eos_id=None):
+    dec = FullDecoder(model, prompt, gen_len, k, eos_id=eos_id)
     recs = []
     while not dec.done():
         recs.append(dec.step(override, keep_logits))
@@ -242,7 +294,7 @@ class PlannedStep:
 
 
 def plan_counts(n_prompt: int, gen_len: int, win: synth.WindowSettings) -> List[PlannedStep]:
-    """Every count of the schedule, derived from counts alone.
+    """Every count of the schedule without adaptive termination, from counts alone.
 
     The counts do not depend on which positions get decoded: |A| is
     min(n_active, undecoded left in W_ex), each step decodes min(k, |A|), and

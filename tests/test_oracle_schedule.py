@@ -300,3 +300,152 @@ def test_full_decoder_candidates_are_all_masked():
     dec = FullDecoder(m, [1, 2], 6, 2)
     rec = dec.step()
     assert rec.active == list(range(2, 8)) and len(rec.selected) == 2
+
+
+# ---- adaptive termination at <eos> -------------------------------------------------------
+
+EOS_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "eos_walkthrough.txt")
+EOS = 5   # <eos> id of the walk-throughs (StubModel vocabulary of 24)
+
+
+def load_eos_golden():
+    cases, cur = [], None
+    for line in open(EOS_GOLDEN):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        f = line.split()
+        if f[0] == "case":
+            cur = {"name": f[1], "args": [int(v) for v in f[2:8]],
+                   "eos_steps": [int(v) for v in f[8].split(",")], "rows": []}
+        elif f[0] == "end":
+            cases.append(cur)
+        else:
+            cur["rows"].append(f)
+    return cases
+
+
+def rightmost_with_eos(k, eos_steps, eos=EOS):
+    def pick(rec):
+        sel = sorted(rec.active)[::-1][:k]
+        toks = {p: 1 for p in sel}
+        if rec.t in eos_steps and sel:
+            toks[sel[0]] = eos
+        return sel, toks
+    return pick
+
+
+@pytest.mark.parametrize("case", load_eos_golden(), ids=lambda c: c["name"])
+def test_eos_hand_walkthrough(case):
+    n_p, G, na, nb, R, k = case["args"]
+    win = synth.WindowSettings(na, nb, R, k)
+    dec = WindowedDecoder(StubModel(), list(range(n_p)), G, win, eos_id=EOS)
+    pick = rightmost_with_eos(k, case["eos_steps"])
+    for row in case["rows"]:
+        t, refresh, ctx = int(row[0]), bool(int(row[1])), int(row[2])
+        assert not dec.done()
+        rec = dec.step(override=pick)
+        assert rec.t == t and rec.refresh == refresh and rec.ctx_len == ctx
+        assert rec.window == _parse_set(row[3])
+        assert rec.active == _parse_set(row[4])
+        assert sorted(rec.phase_decoded) == _parse_set(row[5])
+        buf = [p for p in rec.window
+               if p not in rec.active and p not in rec.phase_decoded and p < ctx]
+        assert buf == _parse_set(row[6])
+        assert rec.online == _parse_set(row[7])
+        assert rec.selected == _parse_set(row[8])
+    assert dec.done()
+    # past the end only tokens decoded before the end moved there remain; every
+    # other position keeps the mask token
+    past = dec.decoded[dec.end:]
+    assert (dec.x[dec.end:][~past] == dec.model.shape.mask_id).all()
+    assert past.sum() == (1 if case["name"] == "F" else 0)
+
+
+@settings_small
+@given(n_p=st.integers(1, 10), G=st.integers(1, 40), na=st.integers(1, 8),
+       nb=st.integers(0, 10), R=st.integers(1, 8), k=st.integers(1, 3), seed=st.integers(0, 99),
+       eos_steps=st.sets(st.integers(0, 30), max_size=3))
+def test_eos_invariants(n_p, G, na, nb, R, k, seed, eos_steps):
+    """Whatever steps write <eos>: nothing at or after the end is ever computed
+    again, the schedule finishes exactly the live prefix, and it never takes
+    more steps than decoding without <eos>."""
+    win = synth.WindowSettings(na, nb, R, k)
+    rng = np.random.default_rng(seed)
+
+    def pick(rec):
+        n = min(k, len(rec.active))
+        sel = [int(p) for p in rng.choice(rec.active, size=n, replace=False)]
+        toks = {p: 1 for p in sel}
+        if rec.t in eos_steps:
+            toks[sel[int(rng.integers(len(sel)))]] = EOS
+        return sel, toks
+
+    dec = WindowedDecoder(StubModel(seed=seed), list(range(n_p)), G, win, eos_id=EOS)
+    ends = []
+    steps = 0
+    while not dec.done():
+        end_before = dec.end
+        rec = dec.step(override=pick)
+        steps += 1
+        assert rec.ctx_len <= end_before
+        assert all(p < end_before for p in rec.online)
+        assert all(p < end_before for p in rec.active)
+        assert all(p < end_before for p in rec.phase_decoded)
+        if rec.refresh:
+            assert rec.online == list(range(rec.ctx_len))
+        ends.append(dec.end)
+        assert steps <= G
+    assert ends == sorted(ends, reverse=True)           # the end only moves forward
+    assert dec.decoded[:dec.end].all()
+    mask = dec.model.shape.mask_id
+    assert (dec.x[dec.end:][~dec.decoded[dec.end:]] == mask).all()
+    written = [p for p in range(n_p, dec.S) if dec.decoded[p] and dec.x[p] == EOS]
+    assert dec.end == (min(written) + 1 if written else dec.S)
+    plain = plan_counts(n_p, G, win)
+    assert steps <= len(plain)
+    if not written:
+        assert steps == len(plain)
+
+
+def test_eos_never_written_changes_nothing():
+    m = micro()
+    win = synth.WindowSettings(3, 4, 3, 2)
+    prompt = [3, 9, 27, 1]
+    # an id the trajectory never produces: the run equals the one without <eos>
+    x0, r0 = generate_windowed(m, prompt, 14, win, keep_logits=True)
+    unused = next(v for v in range(m.shape.vocab - 1) if v not in set(x0.tolist()))
+    x1, r1 = generate_windowed(m, prompt, 14, win, keep_logits=True, eos_id=unused)
+    assert (x0 == x1).all() and len(r0) == len(r1)
+    for a, b in zip(r0, r1):
+        assert a.online == b.online and a.ctx_len == b.ctx_len
+        np.testing.assert_array_equal(a.logits, b.logits)
+
+
+@pytest.mark.parametrize("eos_at", [0, 1, 2])
+def test_eos_degenerate_windows_equal_adaptive_full_decoding(eos_at):
+    """With W_ex covering every masked position, a refresh every step and
+    every undecoded position active, the windowed decoder with <eos> is the
+    plain adaptive-length full decoder: a full forward over [0, end) and every
+    live masked position a candidate, at every step."""
+    m = micro()
+    prompt = [5, 17, 33]
+    G, k = 10, 2
+    win = synth.WindowSettings(G, 0, 1, k)
+    eos = 7
+
+    def inject(rec):
+        toks = dict(rec.chosen_tokens)
+        if rec.t == eos_at and rec.selected:
+            toks[rec.selected[-1]] = eos
+        return rec.selected, toks
+
+    xw, rw = generate_windowed(m, prompt, G, win, override=inject, keep_logits=True, eos_id=eos)
+    xf, rf = generate_full(m, prompt, G, k, override=inject, keep_logits=True, eos_id=eos)
+    assert len(rw) == len(rf) and (xw == xf).all()
+    for a, b in zip(rw, rf):
+        assert a.active == b.active and a.ctx_len == b.ctx_len and a.selected == b.selected
+        np.testing.assert_allclose(a.logits, b.logits, rtol=0, atol=1e-12)
+    # the sequence ended before its last position, which was never decoded
+    e = min(p for p in range(len(prompt), len(xw)) if xw[p] == eos)
+    assert e < len(xw) - 1 and xw[-1] == m.shape.mask_id
