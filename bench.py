@@ -14,8 +14,9 @@ Also reported: decoded tokens/s, the speedup over standard full-sequence
 decoding on the same GPU and kernels, the roofline of the dominant kernel
 (the few-row projection GEMM of the normal steps, k_gemm_bf16, timed with HIP
 events on the library's stream; HBM bound), the same for the 128-row-tile GEMM
-of the refresh steps (k_gemm_bf16_big; MFMA bound) and the CPU oracle on a
-bounded sample of the same workload.
+of the refresh steps (k_gemm_bf16_big; MFMA bound), adaptive termination at
+<eos> on the same workload (an <eos> id taken from the fixed-length run) and
+the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -196,6 +197,75 @@ def generation(model, prompts, G, wc, n_steps, full=False):
     gen.free()  # synchronizes the stream
 
 
+def run_until_done(model, prompts, G, wc):
+    """One generation stepped until the library reports it finished; returns
+    (steps taken, seconds, live ends)."""
+    import paper_2601_20332_amd as wd
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    gen = wd.wd_prefill_prompt(model, prompts, G, wc)
+    n = 0
+    while True:
+        st = wd.lib.wd_step(gen.handle, None)
+        if st == wd.WD_ERR_STATE:
+            break
+        wd._check(st)
+        n += 1
+    ends = [int(e) for e in wd.wd_seq_ends(gen)]
+    gen.free()  # synchronizes the stream
+    return n, time.perf_counter() - t0, ends
+
+
+def adaptive_termination(model, prompts, w, n_steps, fixed_s):
+    """Adaptive termination at <eos> (Sec. 4.2) on the same workload.  Random
+    weights never aim at an <eos>, so the <eos> id is the token the fixed-length
+    generation first decodes a quarter of the way through: with it as <eos>
+    the generation ends there.  Also timed: the same tracked path with an id
+    the generation never decodes (no early end), which isolates the cost of
+    reading each step's decisions back."""
+    import numpy as np
+    import paper_2601_20332_amd as wd
+    win = w.window
+    plain = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
+    gen = wd.wd_prefill_prompt(model, prompts, w.gen_len, plain)
+    seen, eos, eos_step = set(), None, None
+    for t in range(n_steps):
+        r = wd.wd_step(gen, want_result=True)
+        toks = [int(x) for x in r.tokens[0] if x >= 0]
+        fresh = [x for x in toks if x not in seen]
+        if eos is None and t >= n_steps // 4 and fresh:
+            eos, eos_step = fresh[0], t
+        seen.update(toks)
+    final = wd.wd_get_state(gen)[0]
+    gen.free()
+    used = set(np.concatenate(final).tolist())
+    unused = next(v for v in range(w.model.vocab - 1) if v not in used)
+
+    def timed(eos_id, reps=2):
+        wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every,
+                              win.unmask_per_step, eos_id=eos_id)
+        run_until_done(model, prompts, w.gen_len, wc)  # warm
+        runs = [run_until_done(model, prompts, w.gen_len, wc) for _ in range(reps)]
+        return runs[0][0], sum(r[1] for r in runs) / reps, runs[0][2]
+
+    n_eos, t_eos, ends = timed(eos)
+    n_none, t_none, _ = timed(unused)
+    return {
+        "eos_token": eos,
+        "eos_first_decoded_at_step": eos_step,
+        "live_end": ends,
+        "seq_len": [len(p) + w.gen_len for p in prompts],
+        "steps": n_eos,
+        "fixed_length_steps": n_steps,
+        "ms_per_generation": round(t_eos * 1e3, 2),
+        "fixed_length_ms_per_generation": round(fixed_s * 1e3, 2),
+        "speedup_vs_fixed_length": round(fixed_s / t_eos, 3),
+        "tracked_no_eos_ms_per_generation": round(t_none * 1e3, 2),
+        "tracking_overhead": round(t_none / fixed_s - 1.0, 4),
+    }
+
+
 def cpu_baseline(w, plan):
     """The float64 oracle on a bounded sample of the workload: one refresh forward
     (the largest retained prefix of the generation) and one normal-step forward
@@ -261,6 +331,8 @@ def main():
                     choices=["llada8b", "dream7b", "llada8b_long", "llada8b_batch16"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full", action="store_true", help="skip the full-sequence comparison")
+    ap.add_argument("--no-eos", action="store_true",
+                    help="skip the adaptive-termination measurement")
     ap.add_argument("--no-events", action="store_true",
                     help="time without the per-launch GEMM events (no roofline)")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
@@ -347,6 +419,10 @@ def main():
         t_full = time.perf_counter() - tf
         full_speedup = round(t_full / (elapsed / args.steps), 3)
         log(f"[bench] full-sequence generation {t_full:.3f}s")
+    adaptive = None
+    if not args.no_eos:
+        adaptive = adaptive_termination(model, prompts, w, n_steps, elapsed / args.steps)
+        log(f"[bench] adaptive termination: {adaptive}")
     model.free()
 
     cpu = None
@@ -388,6 +464,7 @@ def main():
         "speedup_vs_full_sequence": full_speedup,
         "roofline": roofline,
         "roofline_tiled_gemm": roofline_tiled,
+        "adaptive_termination": adaptive,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

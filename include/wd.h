@@ -69,9 +69,23 @@ typedef struct {
 /* Window settings (Sec. 4.2, Sec. 4.3): the internal window holds n_active
  * positions, the external window E = n_active + n_buffer positions; a phase
  * is refresh_every steps (one refresh step, then normal steps); each step
- * decodes unmask_per_step positions. */
+ * decodes unmask_per_step positions.
+ *
+ * stop_at_eos = 0 (the zero-initialized default) turns adaptive termination
+ * off: every position is decoded and eos_id is ignored.  stop_at_eos = 1
+ * turns it on (Sec. 4.2, adaptive termination) with eos_id a token id in
+ * [0, vocab) other than mask_id: once a generated position e of a sequence
+ * is decoded as eos_id, the sequence's live end becomes e + 1 (the first
+ * such position).
+ * Later positions leave the active set, the online rows and the attention
+ * context at once, and phase starts take the window and prefix over
+ * [0, end) only.  The sequence is finished when every position below its
+ * end is decoded; later positions keep mask_id.  Sequences of a batch then
+ * keep their own phase clocks, and the host reads each step's decisions
+ * back (one small synchronization per step). */
 typedef struct {
   int32_t n_active, n_buffer, refresh_every, unmask_per_step;
+  int32_t stop_at_eos, eos_id;
 } wd_window_config;
 
 typedef struct wd_model wd_model; /* opaque: packed weights and model shape */
@@ -84,9 +98,11 @@ typedef struct wd_seq wd_seq;     /* opaque: one batch of sequences being decode
  * Unused entries are set to -1 / -1 / 0. */
 typedef struct {
   int32_t step;        /* index t of the step just taken (0-based) */
-  int32_t is_refresh;  /* 1 if it was the refresh step of a phase */
+  int32_t is_refresh;  /* 1 if it was the refresh step of a phase (of any sequence with
+                          adaptive termination) */
   int32_t n_rows;      /* rows run through the layer stack, summed over the batch */
-  int32_t n_selected;  /* positions decoded per sequence in this step */
+  int32_t n_selected;  /* positions decoded per sequence in this step (the most of any
+                          sequence with adaptive termination) */
   int32_t* positions;
   int32_t* tokens;
   float* conf;
@@ -145,8 +161,9 @@ size_t wd_seq_bytes(const wd_model* m, const wd_window_config* win, int32_t batc
  * cache rows are filled with NaN.  Synchronizes the stream.
  * Errors: WD_ERR_INVALID_ARG (ids outside [0, vocab), NULL pointers,
  * batch outside [1, 64], gen_len < 1, n_active outside [1, 64], n_buffer < 0,
- * refresh_every < 1, unmask_per_step < 1), WD_ERR_OUT_OF_MEMORY (workspace
- * too small), WD_ERR_DEVICE. */
+ * refresh_every < 1, unmask_per_step < 1, stop_at_eos not 0 or 1, or 1
+ * with eos_id not a token id other than mask_id), WD_ERR_OUT_OF_MEMORY
+ * (workspace too small), WD_ERR_DEVICE. */
 wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_t* prompt_lens,
                             int32_t batch, int32_t gen_len, const wd_window_config* win,
                             void* workspace, size_t ws_bytes, wd_seq** out);
@@ -158,14 +175,16 @@ wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_
  * the phase's refresh step.  wd_step calls it by itself when a phase is due
  * (every refresh_every steps, or when a window has no undecoded position
  * left); calling it earlier starts a phase early.  WD_ERR_STATE once every
- * position is decoded, or on a sequence driven by wd_full_step. */
+ * position is decoded, or on a sequence driven by wd_full_step;
+ * WD_ERR_UNSUPPORTED with adaptive termination (there wd_step drives each
+ * sequence's phases). */
 wd_status wd_slide_window(wd_seq* s);
 
 /* Refresh (Sec. 4.3, refresh equation): a full forward over each sequence's
  * retained prefix [0, c) that rewrites the K/V cache rows of every layer and
  * keeps the active rows' final hidden states for the refresh step's logits.
  * Requires a slid phase whose refresh step has not been taken
- * (WD_ERR_STATE otherwise). */
+ * (WD_ERR_STATE otherwise); WD_ERR_UNSUPPORTED with adaptive termination. */
 wd_status wd_refresh_buffer(wd_seq* s);
 
 /* One diffusion step.  If a phase is due it slides and refreshes first.  On
@@ -177,15 +196,26 @@ wd_status wd_refresh_buffer(wd_seq* s);
  * to the lowest id) and the unmask_per_step most confident positions are
  * decoded (ties to the lowest position).  `out` may be NULL (fully
  * asynchronous); otherwise the call synchronizes the stream and fills it.
- * WD_ERR_STATE when every position is already decoded. */
+ * WD_ERR_STATE when every position is already decoded.  With adaptive
+ * termination each unfinished sequence takes its own kind of step (a phase
+ * start with its refresh, or a normal step) within the same launches,
+ * finished sequences take none, and the call always synchronizes;
+ * WD_ERR_STATE once every sequence is finished. */
 wd_status wd_step(wd_seq* s, wd_step_out* out);
 
 /* Standard decoding step (Sec. 3.1) for comparison: a forward over every
  * position of every sequence, logits for every undecoded position, and the
- * unmask_per_step most confident of them decoded.  A sequence is driven
- * either by wd_full_step or by the windowed calls, never both
- * (WD_ERR_STATE). */
+ * unmask_per_step most confident of them decoded.  With adaptive
+ * termination the forward and the candidates of a sequence stop at its live
+ * end.  A sequence is driven either by wd_full_step or by the windowed
+ * calls, never both (WD_ERR_STATE). */
 wd_status wd_full_step(wd_seq* s, wd_step_out* out);
+
+/* Live end of each sequence (batch entries): one past the first generated
+ * position decoded as eos_id, or the sequence length while there is none
+ * (always the sequence length with stop_at_eos = 0).  Host state only: no
+ * synchronization. */
+wd_status wd_seq_ends(const wd_seq* s, int32_t* ends);
 
 /* Synchronizes, then copies the token ids (sum of sequence lengths, sequence
  * after sequence) and the step counter to the host.  `decoded` (same length,

@@ -30,7 +30,7 @@ EXPORTED = ["wd_weight_count", "wd_weight_shape", "wd_model_bytes", "wd_init_mod
             "wd_free_model", "wd_seq_bytes", "wd_prefill_prompt", "wd_slide_window",
             "wd_refresh_buffer", "wd_step", "wd_full_step", "wd_get_state", "wd_debug_logits",
             "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error", "wd_profile_enable",
-            "wd_profile_read"]
+            "wd_profile_read", "wd_seq_ends"]
 
 
 class WdError(RuntimeError):
@@ -50,7 +50,8 @@ class ModelConfig(ctypes.Structure):
 
 class WindowConfig(ctypes.Structure):
     _fields_ = [("n_active", ctypes.c_int32), ("n_buffer", ctypes.c_int32),
-                ("refresh_every", ctypes.c_int32), ("unmask_per_step", ctypes.c_int32)]
+                ("refresh_every", ctypes.c_int32), ("unmask_per_step", ctypes.c_int32),
+                ("stop_at_eos", ctypes.c_int32), ("eos_id", ctypes.c_int32)]
 
 
 class StepOut(ctypes.Structure):
@@ -92,6 +93,7 @@ def _load() -> ctypes.CDLL:
         "wd_step": (i32, [P, ctypes.POINTER(StepOut)]),
         "wd_full_step": (i32, [P, ctypes.POINTER(StepOut)]),
         "wd_get_state": (i32, [P, pi32, ctypes.POINTER(ctypes.c_uint8), pi32]),
+        "wd_seq_ends": (i32, [P, pi32]),
         "wd_debug_logits": (i32, [P, ctypes.POINTER(ctypes.c_float), pi32, i32, pi32]),
         "wd_debug_kv": (i32, [P, i32, i32, ctypes.POINTER(ctypes.c_float),
                               ctypes.POINTER(ctypes.c_float), i32, pi32]),
@@ -132,8 +134,12 @@ def model_config(*, n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab,
                        int(bool(qkv_bias)), rms_eps, rope_theta)
 
 
-def window_config(n_active, n_buffer, refresh_every, unmask_per_step) -> WindowConfig:
-    return WindowConfig(n_active, n_buffer, refresh_every, unmask_per_step)
+def window_config(n_active, n_buffer, refresh_every, unmask_per_step,
+                  eos_id: Optional[int] = None) -> WindowConfig:
+    """eos_id: None keeps adaptive termination off; a token id turns it on."""
+    if eos_id is None:
+        return WindowConfig(n_active, n_buffer, refresh_every, unmask_per_step, 0, -1)
+    return WindowConfig(n_active, n_buffer, refresh_every, unmask_per_step, 1, int(eos_id))
 
 
 # ---- device buffers (torch is plumbing: memory and stream) --------------------------------
@@ -288,6 +294,13 @@ def wd_get_state(gen: Generation):
         out_d.append(dec[o:o + n].astype(bool))
         o += n
     return out_t, out_d, t.value
+
+
+def wd_seq_ends(gen: Generation) -> np.ndarray:
+    """Live end of each sequence (one past its first decoded <eos>, else its length)."""
+    out = np.empty(gen.batch, np.int32)
+    _check(lib.wd_seq_ends(gen.handle, _i32p(out)))
+    return out
 
 
 def wd_debug_logits(gen: Generation):

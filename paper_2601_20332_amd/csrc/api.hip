@@ -5,6 +5,11 @@
 // the device keeps the token state and derives the identities of the rows
 // (build_rows) from the decoded flags.  Nothing is read back between steps
 // unless the caller asks for a step's result.
+//
+// With adaptive termination (eos_id >= 0) the counts depend on where <eos>
+// is decoded, so the host mirrors each sequence's decoded flags (Track),
+// reads every step's decisions back and gives each sequence its own phase
+// clock, window and live end.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -149,6 +154,65 @@ struct Counts {
     in_window -= d;
     dp += d;
     ++j;
+  }
+};
+
+// Exact host copy of one sequence's schedule under adaptive termination
+// (Sec. 4.2): the live end, the decoded flags, the phase's window and its
+// retained prefix.
+struct Track {
+  int n_p = 0, S = 0, end = 0;  // live positions are [0, end)
+  int c = 0;                    // retained prefix of the phase
+  int j = -1;                   // steps taken in the phase (-1: none yet)
+  std::vector<uint8_t> dec, dec0;
+  std::vector<int> window;      // W_ex of the phase
+
+  bool done() const {
+    for (int p = 0; p < end; ++p)
+      if (!dec[p]) return false;
+    return true;
+  }
+  bool live_in_window() const {
+    for (int p : window)
+      if (p < end && !dec[p]) return true;
+    return false;
+  }
+  bool phase_due(int R) const { return j < 0 || j >= R || !live_in_window(); }
+  void slide(int E) {
+    window.clear();
+    c = end;
+    for (int p = 0; p < end; ++p)
+      if (!dec[p]) {
+        window.push_back(p);
+        if ((int)window.size() == E) {
+          c = p + 1;
+          break;
+        }
+      }
+    dec0 = dec;
+    j = 0;
+  }
+  int ctx() const { return std::min(c, end); }
+  int n_active(int na) const {
+    int n = 0;
+    for (int p : window)
+      if (p < end && !dec[p]) ++n;
+    return std::min(n, na);
+  }
+  int n_phase_decoded() const {
+    int n = 0;
+    for (int p = 0; p < ctx(); ++p) n += dec[p] && !dec0[p];
+    return n;
+  }
+  int live_undecoded() const {
+    int n = 0;
+    for (int p = 0; p < end; ++p) n += !dec[p];
+    return n;
+  }
+  // a decision of the step: position p now holds token t
+  void apply(int p, int t, int eos_id) {
+    dec[p] = 1;
+    if (t == eos_id && p >= n_p) end = std::min(end, p + 1);
   }
 };
 
@@ -411,6 +475,9 @@ struct wd_seq {
   bool refreshed = false;
   int mode = 0;  // 0 = not started, 1 = windowed, 2 = full sequence
   int last_nA = 0;
+  // adaptive termination
+  int eos_id = -1;
+  std::vector<Track> tr;
   // device buffers (carved from the caller's workspace)
   int32_t *x, *seq_len, *row_tok, *row_pos, *row_seq, *row_out, *act_pos, *act_tok, *sel_pos,
       *sel_tok, *err;
@@ -509,6 +576,10 @@ bool win_valid(const wd_window_config* w, std::string* why) {
     *why = "n_active above 64 is not supported";
     return false;
   }
+  if (w->stop_at_eos != 0 && w->stop_at_eos != 1) {
+    *why = "stop_at_eos must be 0 or 1";
+    return false;
+  }
   return true;
 }
 
@@ -541,6 +612,10 @@ bool seq_args_valid(const wd_model* m, const wd_window_config* w, int32_t batch,
   }
   if (T > (1L << 24)) {
     *why = "too many positions";
+    return false;
+  }
+  if (w->stop_at_eos && (w->eos_id < 0 || w->eos_id >= m->cfg.vocab || w->eos_id == m->cfg.mask_id)) {
+    *why = "with stop_at_eos, eos_id must be a token id other than mask_id";
     return false;
   }
   if (m->cfg.dtype == WD_DTYPE_F32) {
@@ -666,8 +741,9 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
   return WD_OK;
 }
 
-wd_status forward(wd_seq* s, int mode, const Rows& r) {
-  WD_HIP(wd::build_rows(mode, s->dec, s->dec0, r.n_act, r.g, s->row_tok, s->row_pos, s->row_seq,
+// r.g.mode / r.g.nact give each sequence's rows; r.n_act is the compact stride.
+wd_status forward(wd_seq* s, const Rows& r) {
+  WD_HIP(wd::build_rows(s->dec, s->dec0, r.n_act, r.g, s->row_tok, s->row_pos, s->row_seq,
                         s->row_out, s->act_pos, s->err, s->m->stream));
   if (s->m->cfg.dtype == WD_DTYPE_BF16) return run_layers<uint16_t>(s, r);
   return run_layers<float>(s, r);
@@ -680,6 +756,8 @@ WdStepGeom base_geom(const wd_seq* s) {
   for (int b = 0; b < s->B; ++b) {
     g.off[b] = s->off[b];
     g.ctx[b] = s->ctx.empty() ? s->S[b] : s->ctx[b];
+    g.mode[b] = -1;
+    g.end[b] = s->tr.empty() ? s->S[b] : s->tr[b].end;
   }
   return g;
 }
@@ -709,8 +787,9 @@ wd_status do_slide(wd_seq* s) {
   s->cnt.start_phase();
   for (int b = 0; b < s->B; ++b) s->ctx[b] = s->cnt.ctx(s->S[b]);
   s->refreshed = false;
-  const WdStepGeom g = base_geom(s);
-  WD_HIP(wd::slide(s->dec, s->dec0, s->T, s->cnt.E, g, s->seq_len, s->err, s->m->stream));
+  WdStepGeom g = base_geom(s);
+  for (int b = 0; b < s->B; ++b) g.mode[b] = 0;
+  WD_HIP(wd::slide(s->dec, s->dec0, s->Smax, s->cnt.E, g, s->seq_len, s->err, s->m->stream));
   return WD_OK;
 }
 
@@ -720,12 +799,14 @@ wd_status do_refresh(wd_seq* s) {
   r.n_act = s->cnt.n_active();
   int row = 0;
   for (int b = 0; b < s->B; ++b) {
+    r.g.mode[b] = 0;
+    r.g.nact[b] = r.n_act;
     r.g.row0[b] = row;
     r.g.nrows[b] = s->ctx[b];
     row += s->ctx[b];
   }
   r.M = row;
-  WD_TRY(forward(s, 0, r));
+  WD_TRY(forward(s, r));
   s->refreshed = true;
   return WD_OK;
 }
@@ -736,11 +817,118 @@ wd_status do_normal(wd_seq* s) {
   r.n_act = s->cnt.n_active();
   const int nO = r.n_act + s->cnt.dp;
   for (int b = 0; b < s->B; ++b) {
+    r.g.mode[b] = 1;
+    r.g.nact[b] = r.n_act;
     r.g.row0[b] = b * nO;
     r.g.nrows[b] = nO;
   }
   r.M = s->B * nO;
-  return forward(s, 1, r);
+  return forward(s, r);
+}
+
+// One step under adaptive termination, windowed (full = false) or full
+// sequence: each unfinished sequence takes its own kind of step, then the
+// step's decisions are read back into the host tracks.
+wd_status step_tracked(wd_seq* s, wd_step_out* out, bool full) {
+  const int B = s->B, E = s->win.n_active + s->win.n_buffer, k = s->win.unmask_per_step;
+  Rows r;
+  r.g = base_geom(s);
+  bool any_slide = false, any_refresh = false;
+  int stride = 1, row = 0;
+  for (int b = 0; b < B; ++b) {
+    Track& t = s->tr[b];
+    int mode = -1, na = 0, rows = 0, ctx = 0;
+    if (!t.done()) {
+      if (full) {
+        mode = 2;
+        ctx = t.end;
+        na = t.live_undecoded();
+        rows = ctx;
+      } else {
+        if (t.phase_due(s->win.refresh_every)) {
+          t.slide(E);
+          any_slide = true;
+          mode = 0;
+          rows = t.c;
+        } else {
+          mode = 1;
+        }
+        ctx = t.ctx();
+        na = t.n_active(s->win.n_active);
+        if (mode == 1) rows = na + t.n_phase_decoded();
+      }
+    }
+    any_refresh |= mode == 0 || mode == 2;
+    s->ctx[b] = ctx;
+    r.g.ctx[b] = ctx;
+    r.g.mode[b] = mode;
+    r.g.nact[b] = na;
+    r.g.row0[b] = row;
+    r.g.nrows[b] = rows;
+    row += rows;
+    stride = std::max(stride, na);
+  }
+  if (any_slide) {
+    WdStepGeom g = r.g;
+    for (int b = 0; b < B; ++b) g.ctx[b] = s->tr[b].c;
+    WD_HIP(wd::slide(s->dec, s->dec0, s->Smax, E, g, s->seq_len, s->err, s->m->stream));
+  }
+  r.M = row;
+  r.n_act = stride;
+  WD_TRY(forward(s, r));
+  WD_TRY(decide(s, stride));
+  const int step = s->t;
+  s->t++;
+  // the decisions, read back every step
+  hipStream_t st = s->m->stream;
+  WD_HIP(hipMemcpyAsync(s->h_buf, s->sel_pos, B * k * 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipMemcpyAsync(s->h_buf + B * k, s->sel_tok, B * k * 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipMemcpyAsync(s->h_buf + 2 * B * k, s->sel_conf, B * k * 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipMemcpyAsync(s->h_buf + 3 * B * k, s->err, 4, hipMemcpyDeviceToHost, st));
+  WD_HIP(hipStreamSynchronize(st));
+  if (s->h_buf[3 * B * k] != 0)
+    return fail(WD_ERR_DEVICE, "device bookkeeping disagrees with the schedule (code %d)",
+                s->h_buf[3 * B * k]);
+  int nsel = 0;
+  for (int b = 0; b < B; ++b) {
+    Track& t = s->tr[b];
+    if (r.g.mode[b] < 0) continue;
+    // checked against the state before the step (a step may decode an <eos>
+    // and, in the same step, a later position), then applied
+    int n = 0;
+    for (int i = 0; i < k; ++i) {
+      const int p = s->h_buf[b * k + i];
+      if (p < 0) continue;
+      if (p >= t.end || t.dec[p])
+        return fail(WD_ERR_DEVICE, "device decoded position %d of sequence %d out of turn", p, b);
+      ++n;
+    }
+    for (int i = 0; i < k; ++i) {
+      const int p = s->h_buf[b * k + i];
+      if (p >= 0) t.apply(p, s->h_buf[B * k + b * k + i], s->eos_id);
+    }
+    if (n != std::min(k, r.g.nact[b]))
+      return fail(WD_ERR_DEVICE, "sequence %d decoded %d positions, expected %d", b, n,
+                  std::min(k, r.g.nact[b]));
+    nsel = std::max(nsel, n);
+    if (!full) t.j++;
+  }
+  if (out) {
+    out->step = step;
+    out->is_refresh = any_refresh ? 1 : 0;
+    out->n_rows = row;
+    out->n_selected = nsel;
+    if (out->positions) memcpy(out->positions, s->h_buf, B * k * 4);
+    if (out->tokens) memcpy(out->tokens, s->h_buf + B * k, B * k * 4);
+    if (out->conf) memcpy(out->conf, s->h_buf + 2 * B * k, B * k * 4);
+  }
+  return WD_OK;
+}
+
+bool all_done(const wd_seq* s) {
+  for (const Track& t : s->tr)
+    if (!t.done()) return false;
+  return true;
 }
 
 wd_status fetch_out(wd_seq* s, wd_step_out* out, int step, int refresh, int rows, int nsel) {
@@ -855,6 +1043,17 @@ wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_
   s->A_max = L.A_max;
   s->C_floats = L.C_floats;
 
+  s->eos_id = win->stop_at_eos ? win->eos_id : -1;
+  if (s->eos_id >= 0)
+    for (int b = 0; b < batch; ++b) {
+      Track t;
+      t.n_p = prompt_lens[b];
+      t.S = t.end = prompt_lens[b] + gen_len;
+      t.dec.assign(t.S, 0);
+      std::fill(t.dec.begin(), t.dec.begin() + t.n_p, 1);
+      t.dec0 = t.dec;
+      s->tr.push_back(std::move(t));
+    }
   s->cnt.E = win->n_active + win->n_buffer;
   s->cnt.R = win->refresh_every;
   s->cnt.k = win->unmask_per_step;
@@ -911,6 +1110,8 @@ wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_
 
 wd_status wd_slide_window(wd_seq* s) {
   if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
+  if (s->eos_id >= 0)
+    return fail(WD_ERR_UNSUPPORTED, "with adaptive termination phases are driven by wd_step");
   if (s->mode == 2) return fail(WD_ERR_STATE, "sequence is driven by wd_full_step");
   if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
   s->mode = 1;
@@ -919,6 +1120,8 @@ wd_status wd_slide_window(wd_seq* s) {
 
 wd_status wd_refresh_buffer(wd_seq* s) {
   if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
+  if (s->eos_id >= 0)
+    return fail(WD_ERR_UNSUPPORTED, "with adaptive termination phases are driven by wd_step");
   if (s->mode == 2) return fail(WD_ERR_STATE, "sequence is driven by wd_full_step");
   if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
   if (s->cnt.j != 0 || s->refreshed)
@@ -930,6 +1133,11 @@ wd_status wd_refresh_buffer(wd_seq* s) {
 wd_status wd_step(wd_seq* s, wd_step_out* out) {
   if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
   if (s->mode == 2) return fail(WD_ERR_STATE, "sequence is driven by wd_full_step");
+  if (s->eos_id >= 0) {
+    if (all_done(s)) return fail(WD_ERR_STATE, "every live position is decoded");
+    s->mode = 1;
+    return step_tracked(s, out, false);
+  }
   if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
   s->mode = 1;
   if (s->cnt.phase_due()) WD_TRY(do_slide(s));
@@ -956,18 +1164,25 @@ wd_status wd_step(wd_seq* s, wd_step_out* out) {
 wd_status wd_full_step(wd_seq* s, wd_step_out* out) {
   if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
   if (s->mode == 1) return fail(WD_ERR_STATE, "sequence is driven by the windowed calls");
+  if (s->eos_id >= 0) {
+    if (all_done(s)) return fail(WD_ERR_STATE, "every live position is decoded");
+    s->mode = 2;
+    return step_tracked(s, out, true);
+  }
   if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
   s->mode = 2;
   Rows r;
   for (int b = 0; b < s->B; ++b) s->ctx[b] = s->S[b];
   r.g = base_geom(s);
   for (int b = 0; b < s->B; ++b) {
+    r.g.mode[b] = 2;
+    r.g.nact[b] = s->cnt.u;
     r.g.row0[b] = s->off[b];
     r.g.nrows[b] = s->S[b];
   }
   r.M = (int)s->T;
   r.n_act = s->cnt.u;
-  WD_TRY(forward(s, 2, r));
+  WD_TRY(forward(s, r));
   const int nA = s->cnt.u;
   const int nsel = std::min(s->cnt.k, nA);
   WD_TRY(decide(s, nA));
@@ -985,6 +1200,12 @@ wd_status wd_get_state(const wd_seq* s, int32_t* tokens, uint8_t* decoded, int32
   WD_HIP(hipMemcpy(tokens, s->x, s->T * 4, hipMemcpyDeviceToHost));
   if (decoded) WD_HIP(hipMemcpy(decoded, s->dec, s->T, hipMemcpyDeviceToHost));
   if (t) *t = s->t;
+  return WD_OK;
+}
+
+wd_status wd_seq_ends(const wd_seq* s, int32_t* ends) {
+  if (!s || !ends) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  for (int b = 0; b < s->B; ++b) ends[b] = s->tr.empty() ? s->S[b] : s->tr[b].end;
   return WD_OK;
 }
 

@@ -116,8 +116,11 @@ __device__ __forceinline__ float block_sum(float v, float* red /* >= 16 floats o
 #define WD_MAX_BATCH 64
 struct WdStepGeom {
   int32_t batch;
-  int32_t ctx[WD_MAX_BATCH];    // retained prefix length c of each sequence
+  int32_t ctx[WD_MAX_BATCH];    // attended prefix length of each sequence this step
   int32_t row0[WD_MAX_BATCH];   // first row of each sequence in this step's row set
   int32_t nrows[WD_MAX_BATCH];  // rows of each sequence in this step's row set
   int32_t off[WD_MAX_BATCH];    // first token of each sequence in the token / K/V arrays
+  int32_t mode[WD_MAX_BATCH];   // rows of the sequence: 0 refresh, 1 normal, 2 full, -1 none
+  int32_t nact[WD_MAX_BATCH];   // active positions of the sequence this step
+  int32_t end[WD_MAX_BATCH];    // live end: S, or one past the first decoded <eos>
 };

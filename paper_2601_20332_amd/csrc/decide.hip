@@ -119,12 +119,16 @@ __device__ __forceinline__ int block_prefix(bool f, int* wtot, int& total) {
 // ---- row set of a step ----------------------------------------------------------------------
 // One workgroup per sequence walks positions [0, c) in order, so rows come
 // out sorted by position.  Active positions are the first n_act undecoded
-// ones (the internal window); rows:
-//   mode 0 (refresh): every position of [0, c), row = row0 + p
-//   mode 1 (normal):  active positions and positions decoded in the phase
-//   mode 2 (full):    every position of [0, S), every undecoded one active
+// ones (the internal window); rows, by the sequence's mode g.mode[b]:
+//   0 (refresh): every position of [0, c), row = row0 + p
+//   1 (normal):  active positions and positions decoded in the phase
+//   2 (full):    every position of [0, c), every undecoded one active
+//  -1:           none (a finished sequence)
+// c = g.ctx[b].  Sequence b has g.nact[b] active positions, stored at
+// compact indices b * n_act + rank (n_act = the stride, at least every
+// g.nact[b]); unused slots get position -1.
 // err bit 0: the row or active count differs from the host's schedule.
-__global__ __launch_bounds__(1024) void k_build_rows(int mode, const uint8_t* __restrict__ dec,
+__global__ __launch_bounds__(1024) void k_build_rows(const uint8_t* __restrict__ dec,
                                                      const uint8_t* __restrict__ dec0, int n_act,
                                                      WdStepGeom g, int32_t* __restrict__ row_tok,
                                                      int32_t* __restrict__ row_pos,
@@ -134,7 +138,8 @@ __global__ __launch_bounds__(1024) void k_build_rows(int mode, const uint8_t* __
                                                      int32_t* __restrict__ err) {
   __shared__ int wtot[16];
   const int b = blockIdx.x;
-  const int off = g.off[b], c = g.ctx[b], row0 = g.row0[b], nrows = g.nrows[b];
+  const int mode = g.mode[b], na = g.nact[b];
+  const int off = g.off[b], c = mode < 0 ? 0 : g.ctx[b], row0 = g.row0[b], nrows = g.nrows[b];
   int carry_u = 0, carry_o = 0;
   for (int base = 0; base < c; base += blockDim.x) {
     const int p = base + threadIdx.x;
@@ -143,7 +148,7 @@ __global__ __launch_bounds__(1024) void k_build_rows(int mode, const uint8_t* __
     const bool und = valid && !d;
     int tot_u, tot_o;
     const int rank_u = carry_u + block_prefix(und, wtot, tot_u);
-    const bool act = und && rank_u < n_act;
+    const bool act = und && rank_u < na;
     bool online;
     if (mode == 1)
       online = act || (valid && d && dec0[off + p] == 0);
@@ -172,34 +177,41 @@ __global__ __launch_bounds__(1024) void k_build_rows(int mode, const uint8_t* __
     row_seq[row0 + i] = b;
     row_out[row0 + i] = -1;
   }
-  for (int i = carry_u + threadIdx.x; i < n_act; i += blockDim.x) act_pos[b * n_act + i] = -1;
+  for (int i = min(carry_u, na) + threadIdx.x; i < n_act; i += blockDim.x) act_pos[b * n_act + i] = -1;
   if (threadIdx.x == 0) {
-    if (wrote_o != nrows || carry_u < n_act) atomicOr(err, 1);
+    if (wrote_o != nrows || carry_u < na || na > n_act) atomicOr(err, 1);
   }
 }
 
-hipError_t build_rows(int mode, const uint8_t* decoded, const uint8_t* decoded0, int n_act,
+hipError_t build_rows(const uint8_t* decoded, const uint8_t* decoded0, int n_act,
                       const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos, int32_t* row_seq,
                       int32_t* row_out, int32_t* act_pos, int32_t* err, hipStream_t st) {
-  hipLaunchKernelGGL(k_build_rows, dim3(g.batch), dim3(1024), 0, st, mode, decoded, decoded0,
-                     n_act, g, row_tok, row_pos, row_seq, row_out, act_pos, err);
+  hipLaunchKernelGGL(k_build_rows, dim3(g.batch), dim3(1024), 0, st, decoded, decoded0, n_act, g,
+                     row_tok, row_pos, row_seq, row_out, act_pos, err);
   return hipGetLastError();
 }
 
 // ---- phase start ------------------------------------------------------------------------------
-__global__ void k_snapshot(const uint8_t* __restrict__ dec, uint8_t* __restrict__ dec0, long n) {
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
-    dec0[i] = dec[i];
+// Sequences with g.mode[b] == 0 start a phase: their decoded flags are
+// snapshot (D_p is measured against it) and their window is checked.
+__global__ void k_snapshot(const uint8_t* __restrict__ dec, uint8_t* __restrict__ dec0, WdStepGeom g,
+                           const int32_t* __restrict__ seq_len) {
+  const int b = blockIdx.y;
+  if (g.mode[b] != 0) return;
+  const long off = g.off[b];
+  for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < seq_len[b]; p += gridDim.x * blockDim.x)
+    dec0[off + p] = dec[off + p];
 }
 
-// err bit 1: c is not (E-th undecoded position + 1), or S when fewer remain.
+// err bit 1: c is not (E-th undecoded position below end + 1), or end when
+// fewer remain.
 __global__ __launch_bounds__(1024) void k_check_window(const uint8_t* __restrict__ dec, int E,
                                                        WdStepGeom g,
-                                                       const int32_t* __restrict__ seq_len,
                                                        int32_t* __restrict__ err) {
   __shared__ int red[16];
   const int b = blockIdx.x;
-  const int off = g.off[b], c = g.ctx[b], S = seq_len[b];
+  if (g.mode[b] != 0) return;
+  const int off = g.off[b], c = g.ctx[b], S = g.end[b];
   int below = 0, all = 0;
   for (int p = threadIdx.x; p < S; p += blockDim.x) {
     const int u = dec[off + p] == 0;
@@ -233,11 +245,12 @@ __global__ __launch_bounds__(1024) void k_check_window(const uint8_t* __restrict
   }
 }
 
-hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, long total, int E, const WdStepGeom& g,
+hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, int Smax, int E, const WdStepGeom& g,
                  const int32_t* seq_len, int32_t* err, hipStream_t st) {
-  const int blocks = (int)std::min<long>((total + 255) / 256, 4096);
-  hipLaunchKernelGGL(k_snapshot, dim3(blocks), dim3(256), 0, st, decoded, decoded0, total);
-  hipLaunchKernelGGL(k_check_window, dim3(g.batch), dim3(1024), 0, st, decoded, E, g, seq_len, err);
+  const int chunks = std::max(1, std::min(64, (Smax + 255) / 256));
+  hipLaunchKernelGGL(k_snapshot, dim3(chunks, g.batch), dim3(256), 0, st, decoded, decoded0, g,
+                     seq_len);
+  hipLaunchKernelGGL(k_check_window, dim3(g.batch), dim3(1024), 0, st, decoded, E, g, err);
   return hipGetLastError();
 }
 

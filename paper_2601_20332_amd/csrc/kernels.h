@@ -65,15 +65,16 @@ hipError_t attention_f32(const float* q, const float* kcache, const float* vcach
 constexpr int kConfChunks = 16;
 hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* tok, float* conf,
                       float* scratch, hipStream_t st);
-// Row set of a step.  mode 0 = refresh ([0, c) of each sequence), 1 = normal
-// (active + phase-decoded positions), 2 = full ([0, S) of each sequence,
-// every undecoded position active).  Active rows of sequence b get compact
-// indices b * n_act + rank.
-hipError_t build_rows(int mode, const uint8_t* decoded, const uint8_t* decoded0, int n_act,
+// Row set of a step, per sequence by g.mode[b]: 0 = refresh ([0, c)),
+// 1 = normal (active + phase-decoded positions), 2 = full ([0, c), every
+// undecoded position active), -1 = no rows.  The g.nact[b] active rows of
+// sequence b get compact indices b * n_act + rank.
+hipError_t build_rows(const uint8_t* decoded, const uint8_t* decoded0, int n_act,
                       const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos, int32_t* row_seq,
                       int32_t* row_out, int32_t* act_pos, int32_t* err, hipStream_t st);
-// Phase start: decoded0 = decoded; checks each sequence's c against the flags.
-hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, long total, int E, const WdStepGeom& g,
+// Phase start of the sequences with g.mode[b] == 0: decoded0 = decoded over
+// their positions; checks their c against the flags below g.end[b].
+hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, int Smax, int E, const WdStepGeom& g,
                  const int32_t* seq_len, int32_t* err, hipStream_t st);
 // Top-k decode of each sequence among its n_act candidates; writes tokens,
 // decoded flags and the step's selection (b * k + rank).

@@ -66,9 +66,14 @@ class GpuStep:
 
 
 def run_gpu(model, prompts, gen_len, win: synth.WindowSettings, full: bool = False,
-            max_steps: Optional[int] = None, keep_logits: bool = True) -> List[GpuStep]:
+            max_steps: Optional[int] = None, keep_logits: bool = True,
+            eos_id: Optional[int] = None, ends: Optional[list] = None) -> List[GpuStep]:
+    """Drives a whole generation (or max_steps steps) through the C ABI; with
+    eos_id, adaptive termination is on and `ends` (if given) receives the
+    sequences' live ends."""
     import paper_2601_20332_amd as wd
-    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
+    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step,
+                          eos_id=eos_id)
     gen = wd.wd_prefill_prompt(model, prompts, gen_len, wc)
     steps = []
     try:
@@ -84,6 +89,8 @@ def run_gpu(model, prompts, gen_len, win: synth.WindowSettings, full: bool = Fal
             steps.append(GpuStep(r, lg, pos))
             n += 1
         final = wd.wd_get_state(gen)
+        if ends is not None:
+            ends.extend(int(e) for e in wd.wd_seq_ends(gen))
     finally:
         gen.free()
     return steps, final
@@ -102,13 +109,16 @@ def rel_err(g: np.ndarray, o: np.ndarray) -> np.ndarray:
 
 
 def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuStep], b: int,
-                   batch: int, full: bool = False, max_steps: Optional[int] = None) -> Report:
-    """Replays sequence b of a GPU generation in the oracle and compares every step."""
+                   batch: int, full: bool = False, max_steps: Optional[int] = None,
+                   eos_id: Optional[int] = None, gpu_end: Optional[int] = None) -> Report:
+    """Replays sequence b of a GPU generation in the oracle and compares every step.
+    With eos_id, a sequence the oracle has finished must have no active row and
+    no decision on the GPU either, and the live ends must agree."""
     dtype = om.shape.dtype
     tol = LOGIT_TOL[dtype]
     rep = Report()
-    dec = (FullDecoder(om, prompt, gen_len, win.unmask_per_step) if full
-           else WindowedDecoder(om, prompt, gen_len, win))
+    dec = (FullDecoder(om, prompt, gen_len, win.unmask_per_step, eos_id=eos_id) if full
+           else WindowedDecoder(om, prompt, gen_len, win, eos_id=eos_id))
     for t, gs in enumerate(gpu_steps):
         if max_steps is not None and t >= max_steps:
             break
@@ -116,8 +126,13 @@ def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuSte
         n_act_rows = len(gs.positions) // batch
         g_pos = gs.positions[b * n_act_rows:(b + 1) * n_act_rows]
         g_log = gs.logits[b * n_act_rows:(b + 1) * n_act_rows]
+        live = g_pos >= 0          # unused compact slots hold position -1
+        g_pos, g_log = g_pos[live], g_log[live]
         g_sel = [int(p) for p in gs.res.positions[b] if p >= 0]
         g_tok = {int(p): int(tk) for p, tk in zip(gs.res.positions[b], gs.res.tokens[b]) if p >= 0}
+        if dec.done():
+            assert len(g_pos) == 0 and not g_sel, f"step {t}: finished sequence {b} still decoding"
+            continue
 
         def override(rec):
             assert rec.active == g_pos.tolist(), (t, rec.active, g_pos.tolist())
@@ -159,4 +174,8 @@ def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuSte
 
         dec.step(override=override, keep_logits=True)
         rep.steps += 1
+    if max_steps is None:
+        assert dec.done(), f"sequence {b}: the GPU stopped before the oracle finished"
+    if gpu_end is not None:
+        assert gpu_end == dec.end, f"sequence {b}: live end {gpu_end} vs oracle {dec.end}"
     return rep
