@@ -46,6 +46,15 @@ Adaptive termination (Sec. 4.2, adaptive termination; optional, eos_id):
 * The sequence is finished when every position below end is decoded.  The
   positions after it keep the mask token.
 
+Buffer-only refresh (a variant, not the paper's method; refresh="buffer"):
+
+* The first phase refreshes [0, c) as above.  Every later refresh
+  recomputes only the window W_ex and the positions decoded in the previous
+  phase (D_{p-1}; the one decoded at a phase's last step still holds K/V
+  computed from its [MASK] input), through the same online-row forward as a
+  normal step; the other rows of [0, c) (the prompt and tokens decoded
+  earlier) keep the K/V they were last given.
+
 Readings where the paper is silent:
 
 * A refresh happens at step 0 and then every R steps; a phase also ends
@@ -116,14 +125,20 @@ class WindowedDecoder(_EosEnd):
     """Window-Diffusion decoding of one sequence with the oracle model."""
 
     def __init__(self, model: OracleModel, prompt: Sequence[int], gen_len: int,
-                 win: synth.WindowSettings, eos_id: Optional[int] = None):
+                 win: synth.WindowSettings, eos_id: Optional[int] = None,
+                 refresh: str = "full"):
         if win.n_active < 1 or win.unmask_per_step < 1 or win.refresh_every < 1:
             raise ValueError("window settings must be positive")
         if win.n_buffer < 0 or gen_len < 1:
             raise ValueError("bad window or generation length")
+        if refresh not in ("full", "buffer"):
+            raise ValueError("refresh is 'full' (the paper's) or 'buffer' (variant)")
         self.model = model
         self.win = win
         self.eos_id = eos_id
+        self.refresh_mode = refresh
+        self.phases = 0                     # phases started so far
+        self.prev_phase_decoded: List[int] = []
         self.n_p = len(prompt)
         self.S = self.n_p + gen_len
         self.end = self.S                   # live positions are [0, end)
@@ -154,8 +169,10 @@ class WindowedDecoder(_EosEnd):
         E = self.win.external
         self.window = [int(i) for i in und[:E]]
         self.ctx_len = int(und[E - 1]) + 1 if len(und) >= E else self.end
+        self.prev_phase_decoded = self.phase_decoded
         self.phase_decoded = []
         self.j = 0
+        self.phases += 1
 
     def context(self) -> int:
         """Length of the attended prefix this step."""
@@ -185,13 +202,20 @@ class WindowedDecoder(_EosEnd):
         if refresh:
             self.slide()
             c = self.ctx_len
-            h, Ks, Vs = m.forward(self.x[:c])
-            for l in range(len(Ks)):
-                self.cache.K[l][:c] = Ks[l]
-                self.cache.V[l][:c] = Vs[l]
             A = self.active()
-            rows = list(range(c))
-            hA = h[A]
+            if self.refresh_mode == "buffer" and self.phases > 1:
+                rows = sorted(set(self.window) |
+                              {p for p in self.prev_phase_decoded if p < c})
+                hR = m.forward_rows(self.x[rows], rows, self.cache, c)
+                where = {p: i for i, p in enumerate(rows)}
+                hA = hR[[where[p] for p in A]]
+            else:
+                h, Ks, Vs = m.forward(self.x[:c])
+                for l in range(len(Ks)):
+                    self.cache.K[l][:c] = Ks[l]
+                    self.cache.V[l][:c] = Vs[l]
+                rows = list(range(c))
+                hA = h[A]
         else:
             A = self.active()
             rows = self.online()
@@ -267,8 +291,8 @@ class FullDecoder(_EosEnd):
 
 
 def generate_windowed(model, prompt, gen_len, win, override=None, keep_logits=False,
-                      eos_id=None):
-    dec = WindowedDecoder(model, prompt, gen_len, win, eos_id=eos_id)
+                      eos_id=None, refresh="full"):
+    dec = WindowedDecoder(model, prompt, gen_len, win, eos_id=eos_id, refresh=refresh)
     recs = []
     while not dec.done():
         recs.append(dec.step(override, keep_logits))

@@ -449,3 +449,62 @@ def test_eos_degenerate_windows_equal_adaptive_full_decoding(eos_at):
     # the sequence ended before its last position, which was never decoded
     e = min(p for p in range(len(prompt), len(xw)) if xw[p] == eos)
     assert e < len(xw) - 1 and xw[-1] == m.shape.mask_id
+
+
+# ---- buffer-only refresh (a variant, not the paper's method) -----------------------------
+
+BUF_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "buffer_refresh_walkthrough.txt")
+
+
+def load_buffer_golden():
+    global GOLDEN
+    saved, GOLDEN = GOLDEN, BUF_GOLDEN
+    try:
+        return load_golden()
+    finally:
+        GOLDEN = saved
+
+
+@pytest.mark.parametrize("case", load_buffer_golden(), ids=lambda c: c["name"])
+def test_buffer_refresh_hand_walkthrough(case):
+    n_p, G, na, nb, R, k = case["args"]
+    win = synth.WindowSettings(na, nb, R, k)
+    m = StubModel()
+    dec = WindowedDecoder(m, list(range(n_p)), G, win, refresh="buffer")
+    for row in case["rows"]:
+        t, refresh, ctx = int(row[0]), bool(int(row[1])), int(row[2])
+        rec = dec.step(override=rightmost(k))
+        assert rec.t == t and rec.refresh == refresh and rec.ctx_len == ctx
+        assert rec.window == _parse_set(row[3])
+        assert rec.active == _parse_set(row[4])
+        assert sorted(rec.phase_decoded) == _parse_set(row[5])
+        assert rec.online == _parse_set(row[7])
+        assert rec.selected == _parse_set(row[8])
+        # the model saw exactly the online rows of the step
+        assert m.rows_seen[-1] == rec.online
+    assert dec.done()
+
+
+def test_buffer_refresh_keeps_other_cache_rows_and_matches_full_first_phase():
+    m = micro()
+    win = synth.WindowSettings(3, 3, 3, 1)
+    prompt = [4, 8, 15, 16, 23]
+    G = 12
+    full = WindowedDecoder(m, prompt, G, win)
+    buf = WindowedDecoder(m, prompt, G, win, refresh="buffer")
+    while not full.done():
+        K_before = [k.copy() for k in buf.cache.K]
+        rf = full.step(keep_logits=True)
+        # the variant follows the same decisions, so both runs share one trajectory
+        rb = buf.step(override=lambda rec: (rf.selected, rf.chosen_tokens), keep_logits=True)
+        assert rb.active == rf.active
+        if rb.t < win.refresh_every:
+            # first phase: identical to the paper's refresh
+            np.testing.assert_array_equal(rf.logits, rb.logits)
+        if rb.refresh and rb.t > 0:
+            assert rb.online == sorted(set(rb.window) | set(buf.prev_phase_decoded))
+            untouched = [p for p in range(rb.ctx_len) if p not in rb.online]
+            assert untouched, "some rows must keep their cache"
+            for l in range(m.shape.n_layers):
+                np.testing.assert_array_equal(buf.cache.K[l][untouched], K_before[l][untouched])
+    assert buf.done()
