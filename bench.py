@@ -15,8 +15,9 @@ decoding on the same GPU and kernels, the roofline of the dominant kernel
 (the few-row projection GEMM of the normal steps, k_gemm_bf16, timed with HIP
 events on the library's stream; HBM bound), the same for the 128-row-tile GEMM
 of the refresh steps (k_gemm_bf16_big; MFMA bound), adaptive termination at
-<eos> on the same workload (an <eos> id taken from the fixed-length run) and
-the CPU oracle on a bounded sample of the same workload.
+<eos> on the same workload (an <eos> id taken from the fixed-length run), the
+buffer-only refresh variant (not the paper's method) and the CPU oracle on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -266,6 +267,34 @@ def adaptive_termination(model, prompts, w, n_steps, fixed_s):
     }
 
 
+def buffer_refresh_variant(model, prompts, w, n_steps, fixed_s):
+    """The buffer-only refresh variant (not the paper's method) on the same
+    workload: steps/s and the rows its later refreshes run."""
+    import paper_2601_20332_amd as wd
+    win = w.window
+    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step,
+                          buffer_refresh=True)
+    plan = wd.wd_plan(w.prompt_len, w.gen_len, wc)
+    refresh_rows = [int(r) for r, f in zip(plan["n_rows"], plan["is_refresh"]) if f]
+    generation(model, prompts, w.gen_len, wc, n_steps)  # warm
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    reps = 2
+    for _ in range(reps):
+        generation(model, prompts, w.gen_len, wc, n_steps)
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / reps
+    return {
+        "variant": "buffer-only refresh (not the paper's method)",
+        "steps_per_s": round(n_steps / t, 3),
+        "ms_per_generation": round(t * 1e3, 2),
+        "speedup_vs_paper_refresh": round(fixed_s / t, 3),
+        "refresh_rows_first": refresh_rows[0],
+        "refresh_rows_later_mean": round(sum(refresh_rows[1:]) / max(1, len(refresh_rows) - 1), 1),
+    }
+
+
 def cpu_baseline(w, plan):
     """The float64 oracle on a bounded sample of the workload: one refresh forward
     (the largest retained prefix of the generation) and one normal-step forward
@@ -333,6 +362,8 @@ def main():
     ap.add_argument("--no-full", action="store_true", help="skip the full-sequence comparison")
     ap.add_argument("--no-eos", action="store_true",
                     help="skip the adaptive-termination measurement")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the buffer-only refresh variant")
     ap.add_argument("--no-events", action="store_true",
                     help="time without the per-launch GEMM events (no roofline)")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
@@ -419,6 +450,10 @@ def main():
         t_full = time.perf_counter() - tf
         full_speedup = round(t_full / (elapsed / args.steps), 3)
         log(f"[bench] full-sequence generation {t_full:.3f}s")
+    variant = None
+    if not args.no_variants and len(prompts) == 1:
+        variant = buffer_refresh_variant(model, prompts, w, n_steps, elapsed / args.steps)
+        log(f"[bench] buffer-only refresh variant: {variant}")
     adaptive = None
     if not args.no_eos:
         adaptive = adaptive_termination(model, prompts, w, n_steps, elapsed / args.steps)
@@ -465,6 +500,7 @@ def main():
         "roofline": roofline,
         "roofline_tiled_gemm": roofline_tiled,
         "adaptive_termination": adaptive,
+        "buffer_refresh_variant": variant,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -82,10 +82,18 @@ typedef struct {
  * [0, end) only.  The sequence is finished when every position below its
  * end is decoded; later positions keep mask_id.  Sequences of a batch then
  * keep their own phase clocks, and the host reads each step's decisions
- * back (one small synchronization per step). */
+ * back (one small synchronization per step).
+ *
+ * buffer_refresh = 0 (default) is the paper's refresh (Sec. 4.3): a full
+ * forward over [0, c) at every phase start.  buffer_refresh = 1 selects a
+ * variant that is not the paper's method: the first phase refreshes [0, c);
+ * each later refresh recomputes only the window W_ex and the positions
+ * decoded in the previous phase, and every other row of [0, c) keeps the
+ * K/V it was last given.  Not combinable with stop_at_eos. */
 typedef struct {
   int32_t n_active, n_buffer, refresh_every, unmask_per_step;
   int32_t stop_at_eos, eos_id;
+  int32_t buffer_refresh;
 } wd_window_config;
 
 typedef struct wd_model wd_model; /* opaque: packed weights and model shape */
@@ -162,8 +170,9 @@ size_t wd_seq_bytes(const wd_model* m, const wd_window_config* win, int32_t batc
  * Errors: WD_ERR_INVALID_ARG (ids outside [0, vocab), NULL pointers,
  * batch outside [1, 64], gen_len < 1, n_active outside [1, 64], n_buffer < 0,
  * refresh_every < 1, unmask_per_step < 1, stop_at_eos not 0 or 1, or 1
- * with eos_id not a token id other than mask_id), WD_ERR_OUT_OF_MEMORY
- * (workspace too small), WD_ERR_DEVICE. */
+ * with eos_id not a token id other than mask_id, buffer_refresh not 0 or
+ * 1), WD_ERR_UNSUPPORTED (stop_at_eos with buffer_refresh),
+ * WD_ERR_OUT_OF_MEMORY (workspace too small), WD_ERR_DEVICE. */
 wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_t* prompt_lens,
                             int32_t batch, int32_t gen_len, const wd_window_config* win,
                             void* workspace, size_t ws_bytes, wd_seq** out);
@@ -274,8 +283,10 @@ wd_status wd_profile_read(wd_model* m, int32_t kernel, int64_t* launches, double
 /* The schedule's counts for one sequence, from counts alone (they do not
  * depend on which positions get decoded): for each step t, whether it is a
  * refresh step, the retained prefix length c, |A|, the rows the step runs
- * through the layer stack (c on a refresh step, |A| + |D_p| otherwise) and
- * the positions it decodes.  Writes at most max_steps entries to each
+ * through the layer stack (c on a refresh step, |W_ex| + |D_{p-1}| on the
+ * buffer-only variant's later refreshes, |A| + |D_p| otherwise) and the
+ * positions it decodes.  Adaptive termination is ignored (its counts depend
+ * on where <eos> is decoded).  Writes at most max_steps entries to each
  * non-NULL array and returns the total number of steps, or -1 on invalid
  * arguments.  Needs no GPU. */
 int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, int32_t max_steps,

@@ -317,7 +317,8 @@ class PlannedStep:
     n_decode: int        # positions decoded by this step
 
 
-def plan_counts(n_prompt: int, gen_len: int, win: synth.WindowSettings) -> List[PlannedStep]:
+def plan_counts(n_prompt: int, gen_len: int, win: synth.WindowSettings,
+                refresh: str = "full") -> List[PlannedStep]:
     """Every count of the schedule without adaptive termination, from counts alone.
 
     The counts do not depend on which positions get decoded: |A| is
@@ -331,18 +332,26 @@ def plan_counts(n_prompt: int, gen_len: int, win: synth.WindowSettings) -> List[
     out: List[PlannedStep] = []
     j = None
     in_window = 0
-    dp = 0
+    dp = prev_dp = 0
     c = 0
+    phases = 0
     while u > 0:
-        refresh = j is None or j >= R or in_window == 0
-        if refresh:
+        is_refresh = j is None or j >= R or in_window == 0
+        if is_refresh:
             c = S - u + E if u >= E else S
             in_window = min(E, u)
-            dp = 0
+            prev_dp, dp = dp, 0
             j = 0
+            phases += 1
         n_act = min(na, in_window)
         dec = min(k, n_act)
-        out.append(PlannedStep(refresh, c, n_act, c if refresh else n_act + dp, dp, dec))
+        if not is_refresh:
+            rows = n_act + dp
+        elif refresh == "buffer" and phases > 1:
+            rows = in_window + prev_dp      # W_ex plus the previous phase's decoded positions
+        else:
+            rows = c
+        out.append(PlannedStep(is_refresh, c, n_act, rows, dp, dec))
         in_window -= dec
         dp += dec
         u -= dec

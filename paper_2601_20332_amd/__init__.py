@@ -51,7 +51,8 @@ class ModelConfig(ctypes.Structure):
 class WindowConfig(ctypes.Structure):
     _fields_ = [("n_active", ctypes.c_int32), ("n_buffer", ctypes.c_int32),
                 ("refresh_every", ctypes.c_int32), ("unmask_per_step", ctypes.c_int32),
-                ("stop_at_eos", ctypes.c_int32), ("eos_id", ctypes.c_int32)]
+                ("stop_at_eos", ctypes.c_int32), ("eos_id", ctypes.c_int32),
+                ("buffer_refresh", ctypes.c_int32)]
 
 
 class StepOut(ctypes.Structure):
@@ -135,11 +136,12 @@ def model_config(*, n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab,
 
 
 def window_config(n_active, n_buffer, refresh_every, unmask_per_step,
-                  eos_id: Optional[int] = None) -> WindowConfig:
-    """eos_id: None keeps adaptive termination off; a token id turns it on."""
-    if eos_id is None:
-        return WindowConfig(n_active, n_buffer, refresh_every, unmask_per_step, 0, -1)
-    return WindowConfig(n_active, n_buffer, refresh_every, unmask_per_step, 1, int(eos_id))
+                  eos_id: Optional[int] = None, buffer_refresh: bool = False) -> WindowConfig:
+    """eos_id: None keeps adaptive termination off; a token id turns it on.
+    buffer_refresh selects the buffer-only refresh variant (not the paper's)."""
+    stop, eos = (0, -1) if eos_id is None else (1, int(eos_id))
+    return WindowConfig(n_active, n_buffer, refresh_every, unmask_per_step, stop, eos,
+                        int(bool(buffer_refresh)))
 
 
 # ---- device buffers (torch is plumbing: memory and stream) --------------------------------

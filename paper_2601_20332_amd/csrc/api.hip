@@ -137,15 +137,22 @@ struct Counts {
   int u = 0;          // undecoded positions per sequence
   int in_window = 0;  // undecoded positions of the current window
   int dp = 0;         // positions decoded in the current phase
+  int prev_dp = 0;    // positions decoded in the previous phase
+  int phases = 0;     // phases started
   int j = -1;         // steps taken in the current phase (-1: no phase yet)
 
   bool phase_due() const { return j < 0 || j >= R || in_window == 0; }
   int ctx(int S) const { return u >= E ? S - u + E : S; }
   void start_phase() {
     in_window = std::min(E, u);
+    prev_dp = dp;
     dp = 0;
     j = 0;
+    ++phases;
   }
+  // rows of the refresh step: [0, c), or with the buffer-only variant after
+  // the first phase the window plus the previous phase's decoded positions
+  int refresh_rows(int c, bool buffer) const { return buffer && phases > 1 ? in_window + prev_dp : c; }
   int n_active() const { return std::min(na, in_window); }
   int n_decode() const { return std::min(k, n_active()); }
   void take_step() {
@@ -481,7 +488,7 @@ struct wd_seq {
   // device buffers (carved from the caller's workspace)
   int32_t *x, *seq_len, *row_tok, *row_pos, *row_seq, *row_out, *act_pos, *act_tok, *sel_pos,
       *sel_tok, *err;
-  uint8_t *dec, *dec0;
+  uint8_t *dec, *dec0, *decp;
   float *rope, *h, *C, *logits, *act_conf, *sel_conf, *dbg, *attn_part, *conf_scratch;
   long attn_part_floats = 0;
   void *kc, *vc, *a, *q, *o, *sw, *a_act;
@@ -495,7 +502,7 @@ namespace {
 
 struct SeqLayout {
   size_t total = 0;
-  size_t x, seq_len, dec, dec0, kc, vc, rope, h, a, q, o, sw, C, row_tok, row_pos, row_seq, row_out,
+  size_t x, seq_len, dec, dec0, decp, kc, vc, rope, h, a, q, o, sw, C, row_tok, row_pos, row_seq, row_out,
       act_pos, act_tok, act_conf, a_act, logits, sel_pos, sel_tok, sel_conf, err, dbg, attn_part,
       conf_scratch;
   long M_max, A_max, attn_part_floats;
@@ -530,6 +537,7 @@ SeqLayout seq_layout(const wd_model& m, const wd_window_config& w, int B, long T
   s.seq_len = take(B * 4);
   s.dec = take(T);
   s.dec0 = take(T);
+  s.decp = take(T);
   s.kc = take((size_t)c.n_layers * KVd * T * e);
   s.vc = take((size_t)c.n_layers * KVd * T * e);
   s.rope = take((size_t)Smax * c.head_dim * 4);
@@ -578,6 +586,10 @@ bool win_valid(const wd_window_config* w, std::string* why) {
   }
   if (w->stop_at_eos != 0 && w->stop_at_eos != 1) {
     *why = "stop_at_eos must be 0 or 1";
+    return false;
+  }
+  if (w->buffer_refresh != 0 && w->buffer_refresh != 1) {
+    *why = "buffer_refresh must be 0 or 1";
     return false;
   }
   return true;
@@ -743,8 +755,8 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
 
 // r.g.mode / r.g.nact give each sequence's rows; r.n_act is the compact stride.
 wd_status forward(wd_seq* s, const Rows& r) {
-  WD_HIP(wd::build_rows(s->dec, s->dec0, r.n_act, r.g, s->row_tok, s->row_pos, s->row_seq,
-                        s->row_out, s->act_pos, s->err, s->m->stream));
+  WD_HIP(wd::build_rows(s->dec, s->dec0, s->decp, r.n_act, r.g, s->row_tok, s->row_pos,
+                        s->row_seq, s->row_out, s->act_pos, s->err, s->m->stream));
   if (s->m->cfg.dtype == WD_DTYPE_BF16) return run_layers<uint16_t>(s, r);
   return run_layers<float>(s, r);
 }
@@ -789,7 +801,8 @@ wd_status do_slide(wd_seq* s) {
   s->refreshed = false;
   WdStepGeom g = base_geom(s);
   for (int b = 0; b < s->B; ++b) g.mode[b] = 0;
-  WD_HIP(wd::slide(s->dec, s->dec0, s->Smax, s->cnt.E, g, s->seq_len, s->err, s->m->stream));
+  WD_HIP(wd::slide(s->dec, s->dec0, s->decp, s->Smax, s->cnt.E, g, s->seq_len, s->err,
+                   s->m->stream));
   return WD_OK;
 }
 
@@ -797,13 +810,14 @@ wd_status do_refresh(wd_seq* s) {
   Rows r;
   r.g = base_geom(s);
   r.n_act = s->cnt.n_active();
+  const bool buffer = s->win.buffer_refresh && s->cnt.phases > 1;
   int row = 0;
   for (int b = 0; b < s->B; ++b) {
-    r.g.mode[b] = 0;
+    r.g.mode[b] = buffer ? 3 : 0;
     r.g.nact[b] = r.n_act;
     r.g.row0[b] = row;
-    r.g.nrows[b] = s->ctx[b];
-    row += s->ctx[b];
+    r.g.nrows[b] = s->cnt.refresh_rows(s->ctx[b], s->win.buffer_refresh);
+    row += r.g.nrows[b];
   }
   r.M = row;
   WD_TRY(forward(s, r));
@@ -871,7 +885,7 @@ wd_status step_tracked(wd_seq* s, wd_step_out* out, bool full) {
   if (any_slide) {
     WdStepGeom g = r.g;
     for (int b = 0; b < B; ++b) g.ctx[b] = s->tr[b].c;
-    WD_HIP(wd::slide(s->dec, s->dec0, s->Smax, E, g, s->seq_len, s->err, s->m->stream));
+    WD_HIP(wd::slide(s->dec, s->dec0, s->decp, s->Smax, E, g, s->seq_len, s->err, s->m->stream));
   }
   r.M = row;
   r.n_act = stride;
@@ -977,6 +991,8 @@ wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_
   *out = nullptr;
   if (!seq_args_valid(m, win, batch, prompt_lens, gen_len, &why))
     return fail(WD_ERR_INVALID_ARG, "%s", why.c_str());
+  if (win->stop_at_eos && win->buffer_refresh)
+    return fail(WD_ERR_UNSUPPORTED, "adaptive termination with the buffer-only refresh");
   long n_ids = 0;
   for (int b = 0; b < batch; ++b) n_ids += prompt_lens[b];
   if (n_ids > 0 && !prompt_ids) return fail(WD_ERR_INVALID_ARG, "prompt_ids is NULL");
@@ -1013,6 +1029,7 @@ wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_
   s->seq_len = (int32_t*)(base + L.seq_len);
   s->dec = (uint8_t*)(base + L.dec);
   s->dec0 = (uint8_t*)(base + L.dec0);
+  s->decp = (uint8_t*)(base + L.decp);
   s->kc = base + L.kc;
   s->vc = base + L.vc;
   s->rope = (float*)(base + L.rope);
@@ -1091,6 +1108,7 @@ wd_status wd_prefill_prompt(wd_model* m, const int32_t* prompt_ids, const int32_
   ok = ok && hipMemcpyAsync(s->x, x.data(), T * 4, hipMemcpyHostToDevice, st) == hipSuccess;
   ok = ok && hipMemcpyAsync(s->dec, dec.data(), T, hipMemcpyHostToDevice, st) == hipSuccess;
   ok = ok && hipMemcpyAsync(s->dec0, dec.data(), T, hipMemcpyHostToDevice, st) == hipSuccess;
+  ok = ok && hipMemcpyAsync(s->decp, dec.data(), T, hipMemcpyHostToDevice, st) == hipSuccess;
   ok = ok && hipMemcpyAsync(s->seq_len, s->S.data(), batch * 4, hipMemcpyHostToDevice, st) == hipSuccess;
   ok = ok && hipMemcpyAsync(s->rope, rope.data(), rope.size() * 4, hipMemcpyHostToDevice, st) == hipSuccess;
   ok = ok && hipMemcpyAsync(s->err, &zero, 4, hipMemcpyHostToDevice, st) == hipSuccess;
@@ -1146,7 +1164,7 @@ wd_status wd_step(wd_seq* s, wd_step_out* out) {
   if (refresh) {
     if (!s->refreshed) WD_TRY(do_refresh(s));
     rows = 0;
-    for (int b = 0; b < s->B; ++b) rows += s->ctx[b];
+    for (int b = 0; b < s->B; ++b) rows += s->cnt.refresh_rows(s->ctx[b], s->win.buffer_refresh);
   } else {
     WD_TRY(do_normal(s));
     rows = s->B * (s->cnt.n_active() + s->cnt.dp);
@@ -1287,7 +1305,8 @@ int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, 
       if (is_refresh) is_refresh[t] = refresh ? 1 : 0;
       if (ctx_len) ctx_len[t] = ctx;
       if (n_active) n_active[t] = c.n_active();
-      if (n_rows) n_rows[t] = refresh ? ctx : c.n_active() + c.dp;
+      if (n_rows) n_rows[t] = refresh ? c.refresh_rows(ctx, win->buffer_refresh != 0)
+                                      : c.n_active() + c.dp;
       if (n_decode) n_decode[t] = c.n_decode();
     }
     c.take_step();

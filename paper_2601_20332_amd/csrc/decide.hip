@@ -123,13 +123,18 @@ __device__ __forceinline__ int block_prefix(bool f, int* wtot, int& total) {
 //   0 (refresh): every position of [0, c), row = row0 + p
 //   1 (normal):  active positions and positions decoded in the phase
 //   2 (full):    every position of [0, c), every undecoded one active
+//   3 (buffer-only refresh): undecoded positions of [0, c) and positions
+//                decoded during the previous phase (dec0 set, decp clear)
 //  -1:           none (a finished sequence)
 // c = g.ctx[b].  Sequence b has g.nact[b] active positions, stored at
 // compact indices b * n_act + rank (n_act = the stride, at least every
 // g.nact[b]); unused slots get position -1.
 // err bit 0: the row or active count differs from the host's schedule.
+__device__ __forceinline__ bool compact_mode(int mode) { return mode == 1 || mode == 3; }
+
 __global__ __launch_bounds__(1024) void k_build_rows(const uint8_t* __restrict__ dec,
-                                                     const uint8_t* __restrict__ dec0, int n_act,
+                                                     const uint8_t* __restrict__ dec0,
+                                                     const uint8_t* __restrict__ decp, int n_act,
                                                      WdStepGeom g, int32_t* __restrict__ row_tok,
                                                      int32_t* __restrict__ row_pos,
                                                      int32_t* __restrict__ row_seq,
@@ -152,10 +157,12 @@ __global__ __launch_bounds__(1024) void k_build_rows(const uint8_t* __restrict__
     bool online;
     if (mode == 1)
       online = act || (valid && d && dec0[off + p] == 0);
+    else if (mode == 3)
+      online = und || (valid && d && dec0[off + p] != 0 && decp[off + p] == 0);
     else
       online = valid;
     const int rank_o = carry_o + block_prefix(online, wtot, tot_o);
-    const int ro = mode == 1 ? rank_o : p;
+    const int ro = compact_mode(mode) ? rank_o : p;
     if (online && ro < nrows) {
       const int r = row0 + ro;
       row_tok[r] = off + p;
@@ -170,7 +177,7 @@ __global__ __launch_bounds__(1024) void k_build_rows(const uint8_t* __restrict__
   // A count that disagrees with the host's schedule is reported through err;
   // the slots it left unwritten get harmless values so later kernels stay in
   // bounds (position 0 of the sequence, no active row).
-  const int wrote_o = mode == 1 ? carry_o : c;
+  const int wrote_o = compact_mode(mode) ? carry_o : c;
   for (int i = wrote_o + threadIdx.x; i < nrows; i += blockDim.x) {
     row_tok[row0 + i] = off;
     row_pos[row0 + i] = 0;
@@ -183,24 +190,29 @@ __global__ __launch_bounds__(1024) void k_build_rows(const uint8_t* __restrict__
   }
 }
 
-hipError_t build_rows(const uint8_t* decoded, const uint8_t* decoded0, int n_act,
-                      const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos, int32_t* row_seq,
-                      int32_t* row_out, int32_t* act_pos, int32_t* err, hipStream_t st) {
-  hipLaunchKernelGGL(k_build_rows, dim3(g.batch), dim3(1024), 0, st, decoded, decoded0, n_act, g,
-                     row_tok, row_pos, row_seq, row_out, act_pos, err);
+hipError_t build_rows(const uint8_t* decoded, const uint8_t* decoded0, const uint8_t* decoded_prev,
+                      int n_act, const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos,
+                      int32_t* row_seq, int32_t* row_out, int32_t* act_pos, int32_t* err,
+                      hipStream_t st) {
+  hipLaunchKernelGGL(k_build_rows, dim3(g.batch), dim3(1024), 0, st, decoded, decoded0,
+                     decoded_prev, n_act, g, row_tok, row_pos, row_seq, row_out, act_pos, err);
   return hipGetLastError();
 }
 
 // ---- phase start ------------------------------------------------------------------------------
 // Sequences with g.mode[b] == 0 start a phase: their decoded flags are
-// snapshot (D_p is measured against it) and their window is checked.
-__global__ void k_snapshot(const uint8_t* __restrict__ dec, uint8_t* __restrict__ dec0, WdStepGeom g,
+// snapshot (D_p is measured against it; the previous snapshot moves to
+// decp) and their window is checked.
+__global__ void k_snapshot(const uint8_t* __restrict__ dec, uint8_t* __restrict__ dec0,
+                           uint8_t* __restrict__ decp, WdStepGeom g,
                            const int32_t* __restrict__ seq_len) {
   const int b = blockIdx.y;
   if (g.mode[b] != 0) return;
   const long off = g.off[b];
-  for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < seq_len[b]; p += gridDim.x * blockDim.x)
+  for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < seq_len[b]; p += gridDim.x * blockDim.x) {
+    decp[off + p] = dec0[off + p];
     dec0[off + p] = dec[off + p];
+  }
 }
 
 // err bit 1: c is not (E-th undecoded position below end + 1), or end when
@@ -245,11 +257,11 @@ __global__ __launch_bounds__(1024) void k_check_window(const uint8_t* __restrict
   }
 }
 
-hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, int Smax, int E, const WdStepGeom& g,
-                 const int32_t* seq_len, int32_t* err, hipStream_t st) {
+hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, uint8_t* decoded_prev, int Smax, int E,
+                 const WdStepGeom& g, const int32_t* seq_len, int32_t* err, hipStream_t st) {
   const int chunks = std::max(1, std::min(64, (Smax + 255) / 256));
-  hipLaunchKernelGGL(k_snapshot, dim3(chunks, g.batch), dim3(256), 0, st, decoded, decoded0, g,
-                     seq_len);
+  hipLaunchKernelGGL(k_snapshot, dim3(chunks, g.batch), dim3(256), 0, st, decoded, decoded0,
+                     decoded_prev, g, seq_len);
   hipLaunchKernelGGL(k_check_window, dim3(g.batch), dim3(1024), 0, st, decoded, E, g, err);
   return hipGetLastError();
 }

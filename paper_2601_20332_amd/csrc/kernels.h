@@ -67,15 +67,18 @@ hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* t
                       float* scratch, hipStream_t st);
 // Row set of a step, per sequence by g.mode[b]: 0 = refresh ([0, c)),
 // 1 = normal (active + phase-decoded positions), 2 = full ([0, c), every
-// undecoded position active), -1 = no rows.  The g.nact[b] active rows of
-// sequence b get compact indices b * n_act + rank.
-hipError_t build_rows(const uint8_t* decoded, const uint8_t* decoded0, int n_act,
-                      const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos, int32_t* row_seq,
-                      int32_t* row_out, int32_t* act_pos, int32_t* err, hipStream_t st);
-// Phase start of the sequences with g.mode[b] == 0: decoded0 = decoded over
-// their positions; checks their c against the flags below g.end[b].
-hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, int Smax, int E, const WdStepGeom& g,
-                 const int32_t* seq_len, int32_t* err, hipStream_t st);
+// undecoded position active), 3 = buffer-only refresh (undecoded positions
+// of [0, c) + positions decoded in the previous phase), -1 = no rows.  The
+// g.nact[b] active rows of sequence b get compact indices b * n_act + rank.
+hipError_t build_rows(const uint8_t* decoded, const uint8_t* decoded0, const uint8_t* decoded_prev,
+                      int n_act, const WdStepGeom& g, int32_t* row_tok, int32_t* row_pos,
+                      int32_t* row_seq, int32_t* row_out, int32_t* act_pos, int32_t* err,
+                      hipStream_t st);
+// Phase start of the sequences with g.mode[b] == 0: decoded_prev = decoded0,
+// decoded0 = decoded over their positions; checks their c against the flags
+// below g.end[b].
+hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, uint8_t* decoded_prev, int Smax, int E,
+                 const WdStepGeom& g, const int32_t* seq_len, int32_t* err, hipStream_t st);
 // Top-k decode of each sequence among its n_act candidates; writes tokens,
 // decoded flags and the step's selection (b * k + rank).
 hipError_t select_update(const int32_t* act_pos, const int32_t* act_tok, const float* act_conf,

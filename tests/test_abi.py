@@ -110,10 +110,11 @@ def test_plan_rejects_bad_windows():
         wd.wd_plan(4, 0, wd.window_config(2, 2, 2, 1))
 
 
-def _compare_plan(n_p, G, win):
-    ref = plan_counts(n_p, G, win)
+def _compare_plan(n_p, G, win, refresh="full"):
+    ref = plan_counts(n_p, G, win, refresh=refresh)
     got = wd.wd_plan(n_p, G, wd.window_config(win.n_active, win.n_buffer, win.refresh_every,
-                                              win.unmask_per_step))
+                                              win.unmask_per_step,
+                                              buffer_refresh=refresh == "buffer"))
     assert len(got["n_rows"]) == len(ref)
     assert got["is_refresh"].tolist() == [int(p.refresh) for p in ref]
     assert got["ctx_len"].tolist() == [p.ctx_len for p in ref]
@@ -134,3 +135,12 @@ def test_plan_matches_oracle_on_workloads(name):
        nb=st.integers(0, 70), R=st.integers(1, 20), k=st.integers(1, 8))
 def test_plan_matches_oracle_everywhere(n_p, G, na, nb, R, k):
     _compare_plan(n_p, G, synth.WindowSettings(na, nb, R, k))
+    _compare_plan(n_p, G, synth.WindowSettings(na, nb, R, k), refresh="buffer")
+
+
+def test_plan_rejects_bad_variant_flags():
+    for field in ("stop_at_eos", "buffer_refresh"):
+        win = wd.window_config(2, 2, 2, 1)
+        setattr(win, field, 2)
+        with pytest.raises(wd.WdError):
+            wd.wd_plan(4, 8, win)

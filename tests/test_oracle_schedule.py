@@ -107,14 +107,15 @@ settings_small = settings(max_examples=120, deadline=None)
 @settings_small
 @given(n_p=st.integers(1, 12), G=st.integers(1, 60), na=st.integers(1, 9),
        nb=st.integers(0, 12), R=st.integers(1, 9), k=st.integers(1, 4), seed=st.integers(0, 99))
-def test_counts_closed_form_and_invariants(n_p, G, na, nb, R, k, seed):
+@pytest.mark.parametrize("refresh", ["full", "buffer"])
+def test_counts_closed_form_and_invariants(n_p, G, na, nb, R, k, seed, refresh):
     """plan_counts (counts only) equals the trajectory's counts for any decode
     order; roles partition W_ex; the active window only moves right; no
     far-field position is ever computed."""
     win = synth.WindowSettings(na, nb, R, k)
     m = StubModel(seed=seed)
-    dec = WindowedDecoder(m, list(range(n_p)), G, win)
-    plan = plan_counts(n_p, G, win)
+    dec = WindowedDecoder(m, list(range(n_p)), G, win, refresh=refresh)
+    plan = plan_counts(n_p, G, win, refresh=refresh)
     recs = []
     prev_active = None
     while not dec.done():

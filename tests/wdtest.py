@@ -67,13 +67,14 @@ class GpuStep:
 
 def run_gpu(model, prompts, gen_len, win: synth.WindowSettings, full: bool = False,
             max_steps: Optional[int] = None, keep_logits: bool = True,
-            eos_id: Optional[int] = None, ends: Optional[list] = None) -> List[GpuStep]:
+            eos_id: Optional[int] = None, ends: Optional[list] = None,
+            refresh: str = "full") -> List[GpuStep]:
     """Drives a whole generation (or max_steps steps) through the C ABI; with
     eos_id, adaptive termination is on and `ends` (if given) receives the
     sequences' live ends."""
     import paper_2601_20332_amd as wd
     wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step,
-                          eos_id=eos_id)
+                          eos_id=eos_id, buffer_refresh=refresh == "buffer")
     gen = wd.wd_prefill_prompt(model, prompts, gen_len, wc)
     steps = []
     try:
@@ -110,7 +111,8 @@ def rel_err(g: np.ndarray, o: np.ndarray) -> np.ndarray:
 
 def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuStep], b: int,
                    batch: int, full: bool = False, max_steps: Optional[int] = None,
-                   eos_id: Optional[int] = None, gpu_end: Optional[int] = None) -> Report:
+                   eos_id: Optional[int] = None, gpu_end: Optional[int] = None,
+                   refresh: str = "full") -> Report:
     """Replays sequence b of a GPU generation in the oracle and compares every step.
     With eos_id, a sequence the oracle has finished must have no active row and
     no decision on the GPU either, and the live ends must agree."""
@@ -118,7 +120,7 @@ def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuSte
     tol = LOGIT_TOL[dtype]
     rep = Report()
     dec = (FullDecoder(om, prompt, gen_len, win.unmask_per_step, eos_id=eos_id) if full
-           else WindowedDecoder(om, prompt, gen_len, win, eos_id=eos_id))
+           else WindowedDecoder(om, prompt, gen_len, win, eos_id=eos_id, refresh=refresh))
     for t, gs in enumerate(gpu_steps):
         if max_steps is not None and t >= max_steps:
             break
