@@ -63,10 +63,12 @@ def measured_traffic(kernel: str):
 
 
 def kernel_class_of(name: str):
-    """WD_PROF_* class of a kernel name as rocprofv3 prints it."""
+    """WD_PROF_* class of a kernel name as rocprofv3 prints it: the few-row
+    products (k_gemm_bf16, and k_gemm_bf16_fused that carries the Q/K/V or
+    SwiGLU epilogue) or the 128-row-tile kernel."""
     if "k_gemm_bf16_big<" in name:
         return 2
-    if "k_gemm_bf16<" in name:
+    if "k_gemm_bf16<" in name or "k_gemm_bf16_fused<" in name:
         return 1
     return None
 
@@ -151,7 +153,7 @@ def roofline_of(model, kernel_class: int, elapsed_ev: float):
     hbm = kernel_class == 1
     achieved, peak = (gbs, HBM_PEAK_GBS) if hbm else (tfs, BF16_PEAK_TFLOPS)
     return {
-        "kernel": name,
+        "kernel": name + (" + k_gemm_bf16_fused (at most 64 rows)" if hbm else " (128-row tiles)"),
         "bound": "hbm" if hbm else "mfma",
         "achieved": round(achieved, 1),
         "peak": peak,

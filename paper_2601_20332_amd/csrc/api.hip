@@ -297,11 +297,18 @@ ModelLayout model_layout(const wd_model_config& c) {
 }
 
 // Copies (fp32) or packs into MFMA fragments (bf16) one [N, K] matrix at dst.
-wd_status put_matrix(const wd_model& m, const void* src, long N, long K, char* dst) {
+// bf16 weights are packed into MFMA fragments (rows reordered by perm, W2 =
+// the up half of kPackGateUp); fp32 weights are copied as they are.
+wd_status put_matrix(const wd_model& m, const void* src, long N, long K, char* dst,
+                     int perm = wd::kPackPlain, const void* src2 = nullptr) {
   if (m.cfg.dtype == WD_DTYPE_BF16) {
-    WD_HIP(wd::pack_frags((const uint16_t*)src, (int)N, (int)K, dst, m.stream));
+    WD_HIP(wd::pack_frags((const uint16_t*)src, (int)N, (int)K, dst, m.stream, perm,
+                          (const uint16_t*)src2));
   } else {
-    WD_HIP(hipMemcpyAsync(dst, src, (size_t)N * K * 4, hipMemcpyDeviceToDevice, m.stream));
+    // with src2 (gate then up) each half is N / 2 rows
+    const size_t bytes = (size_t)(src2 ? N / 2 : N) * K * 4;
+    WD_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, m.stream));
+    if (src2) WD_HIP(hipMemcpyAsync(dst + bytes, src2, bytes, hipMemcpyDeviceToDevice, m.stream));
   }
   return WD_OK;
 }
@@ -393,9 +400,11 @@ wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, 
     const void* wq = weights[wi++];
     const void* wk = weights[wi++];
     const void* wv = weights[wi++];
-    if ((st = put_matrix(*m, wq, Q, H, base + L.wqkv)) != WD_OK) return fail_free(st);
-    if ((st = put_matrix(*m, wk, KV, H, base + L.wqkv + Q * H * e)) != WD_OK) return fail_free(st);
-    if ((st = put_matrix(*m, wv, KV, H, base + L.wqkv + (Q + KV) * H * e)) != WD_OK) return fail_free(st);
+    const int rp = wd::kPackRopePair;
+    if ((st = put_matrix(*m, wq, Q, H, base + L.wqkv, rp)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, wk, KV, H, base + L.wqkv + Q * H * e, rp)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, wv, KV, H, base + L.wqkv + (Q + KV) * H * e, rp)) != WD_OK)
+      return fail_free(st);
     if (cfg->qkv_bias) {
       if ((st = copy(weights[wi++], Q * e, base + L.bqkv)) != WD_OK) return fail_free(st);
       if ((st = copy(weights[wi++], KV * e, base + L.bqkv + Q * e)) != WD_OK) return fail_free(st);
@@ -404,8 +413,12 @@ wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, 
     }
     if ((st = put_matrix(*m, weights[wi++], H, Q, base + L.wo)) != WD_OK) return fail_free(st);
     if ((st = copy(weights[wi++], H * e, base + L.ffn_norm)) != WD_OK) return fail_free(st);
-    if ((st = put_matrix(*m, weights[wi++], F, H, base + L.wgu)) != WD_OK) return fail_free(st);
-    if ((st = put_matrix(*m, weights[wi++], F, H, base + L.wgu + F * H * e)) != WD_OK) return fail_free(st);
+    {
+      const void* wg = weights[wi++];
+      const void* wu = weights[wi++];
+      if ((st = put_matrix(*m, wg, 2 * F, H, base + L.wgu, wd::kPackGateUp, wu)) != WD_OK)
+        return fail_free(st);
+    }
     if ((st = put_matrix(*m, weights[wi++], H, F, base + L.wd)) != WD_OK) return fail_free(st);
     w.attn_norm = base + L.attn_norm;
     w.wqkv = base + L.wqkv;
@@ -707,6 +720,14 @@ wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, i
   return profile_end(m, kind, M, N, K, m.esz);
 }
 
+// The few-row products that carry their own epilogue (bf16, at most 64 rows,
+// wide enough for one workgroup per 64 features to fill the GPU).
+bool fused_rows(const wd_model& m, int M, int N, int K) {
+  return m.cfg.dtype == WD_DTYPE_BF16 && wd::fused_rows_ok(M, N, K);
+}
+
+wd_model& m_mut(wd_seq* s) { return *s->m; }
+
 template <typename T>
 wd_status run_layers(wd_seq* s, const Rows& r) {
   const wd_model& m = *s->m;
@@ -725,9 +746,19 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
     const LayerW& w = m.layers[l];
     T* kc = (T*)s->kc + (size_t)l * KVd * s->T;
     T* vc = (T*)s->vc + (size_t)l * KVd * s->T;
-    WD_TRY(gemm<T>(s, a, H, w.wqkv, s->C, M, m.qkv_n, H, 1 << 20, &S));
-    WD_HIP(wd::qkv_epilogue<T>(s->C, S, M, (const T*)w.bqkv, s->rope, s->row_pos, s->row_tok,
-                               c.n_heads, c.n_kv_heads, c.head_dim, q, kc, vc, s->T, st));
+    if (fused_rows(m, M, m.qkv_n, H)) {
+      hipEvent_t e0, e1;
+      WD_TRY(profile_begin(m_mut(s), &e0, &e1));
+      WD_HIP(wd::gemm_bf16_qkv_fused((const uint16_t*)a, H, w.wqkv, M, m.qkv_n, H,
+                                     (const uint16_t*)w.bqkv, s->rope, s->row_pos, s->row_tok,
+                                     c.n_heads, c.n_kv_heads, (uint16_t*)q, (uint16_t*)kc,
+                                     (uint16_t*)vc, s->T, st, e0, e1));
+      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, m.qkv_n, H, m.esz));
+    } else {
+      WD_TRY(gemm<T>(s, a, H, w.wqkv, s->C, M, m.qkv_n, H, 1 << 20, &S));
+      WD_HIP(wd::qkv_epilogue<T>(s->C, S, M, (const T*)w.bqkv, s->rope, s->row_pos, s->row_tok,
+                                 c.n_heads, c.n_kv_heads, c.head_dim, q, kc, vc, s->T, st));
+    }
     if (c.dtype == WD_DTYPE_BF16) {
       WD_HIP(wd::attention_bf16((const uint16_t*)q, (const uint16_t*)kc, (const uint16_t*)vc, s->T,
                                 (uint16_t*)o, r.g, c.n_heads, c.n_kv_heads, c.head_dim,
@@ -739,8 +770,16 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
     }
     WD_TRY(gemm<T>(s, o, Q, w.wo, s->C, M, H, Q, 1 << 20, &S));
     WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)w.ffn_norm, c.rms_eps, a, nullptr, st));
-    WD_TRY(gemm<T>(s, a, H, w.wgu, s->C, M, 2 * F, H, 1 << 20, &S));
-    WD_HIP(wd::swiglu<T>(s->C, S, M, F, sw, st));
+    if (fused_rows(m, M, 2 * F, H)) {
+      hipEvent_t e0, e1;
+      WD_TRY(profile_begin(m_mut(s), &e0, &e1));
+      WD_HIP(wd::gemm_bf16_swiglu_fused((const uint16_t*)a, H, w.wgu, M, F, H, (uint16_t*)sw, st,
+                                        e0, e1));
+      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, 2 * F, H, m.esz));
+    } else {
+      WD_TRY(gemm<T>(s, a, H, w.wgu, s->C, M, 2 * F, H, 1 << 20, &S));
+      WD_HIP(wd::swiglu<T>(s->C, S, M, F, sw, st));
+    }
     WD_TRY(gemm<T>(s, sw, F, w.wd, s->C, M, H, F, 1 << 20, &S));
     if (l + 1 < c.n_layers) {
       WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)m.layers[l + 1].attn_norm,

@@ -18,11 +18,37 @@
 namespace wd {
 
 // ---- weight packing -------------------------------------------------------------
-// Fragment (nt, kt) holds W rows nt*16..nt*16+15 and columns kt*32..kt*32+31;
-// lane l stores row nt*16 + l%16, columns kt*32 + (l/16)*8 .. +7 (the MFMA
-// A-operand layout).  Fragments of one 16-row group are contiguous along K,
-// so a wave streams each group as one contiguous run.
-__global__ void k_pack_frags(const uint16_t* __restrict__ W, int N, int K, u32x4* __restrict__ out) {
+// Fragment (nt, kt) holds packed rows nt*16..nt*16+15 and columns
+// kt*32..kt*32+31; lane l stores packed row nt*16 + l%16, columns
+// kt*32 + (l/16)*8 .. +7 (the MFMA A-operand layout).  Fragments of one
+// 16-row group are contiguous along K, so a wave streams each group as one
+// contiguous run.
+//
+// Row order of the packed matrix (which output feature each packed row is):
+//   kPackPlain:    as given.
+//   kPackRopePair: within each 128-row head, group gi (packed rows
+//                  gi*16..gi*16+15) holds dims gi*8..gi*8+7, then their RoPE
+//                  partners 64+gi*8..64+gi*8+7, so that in the MFMA output a
+//                  value and its partner sit in lanes l and l ^ 32.
+//   kPackGateUp:   W (gate, F rows) and W2 (up, F rows) interleaved: group g
+//                  holds gate features g*8..g*8+7, then the same up features.
+__device__ __forceinline__ long packed_source_row(int perm, long row, int N, int& which) {
+  which = 0;
+  if (perm == kPackRopePair) {
+    const long head = row >> 7;
+    const int r = (int)(row & 127), gi = r >> 4, rr = r & 15;
+    return head * 128 + (rr < 8 ? gi * 8 + rr : 64 + gi * 8 + rr - 8);
+  }
+  if (perm == kPackGateUp) {
+    const int rr = (int)(row & 15);
+    which = rr >= 8;
+    return (row >> 4) * 8 + (rr & 7);
+  }
+  return row;
+}
+
+__global__ void k_pack_frags(const uint16_t* __restrict__ W, const uint16_t* __restrict__ W2, int N,
+                             int K, int perm, u32x4* __restrict__ out) {
   const int KT = K >> 5;
   const long total = (long)(N >> 4) * KT * 64;
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
@@ -31,16 +57,21 @@ __global__ void k_pack_frags(const uint16_t* __restrict__ W, int N, int K, u32x4
     const long f = i >> 6;
     const int kt = (int)(f % KT);
     const long nt = f / KT;
-    const long row = nt * 16 + (lane & 15);
+    int which;
+    const long row = packed_source_row(perm, nt * 16 + (lane & 15), N, which);
     const int col = kt * 32 + (lane >> 4) * 8;
-    out[i] = *(const u32x4*)(W + row * K + col);
+    out[i] = *(const u32x4*)((which ? W2 : W) + row * K + col);
   }
 }
 
-hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st) {
+hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st, int perm,
+                      const uint16_t* W2) {
+  if (N % 16 || K % 32) return hipErrorInvalidValue;
+  if (perm == kPackRopePair && N % 128) return hipErrorInvalidValue;
+  if (perm == kPackGateUp && !W2) return hipErrorInvalidValue;
   const long total = (long)(N / 16) * (K / 32) * 64;
   const int blocks = (int)std::min<long>((total + 255) / 256, 65536);
-  hipLaunchKernelGGL(k_pack_frags, dim3(blocks), dim3(256), 0, st, W, N, K, (u32x4*)out);
+  hipLaunchKernelGGL(k_pack_frags, dim3(blocks), dim3(256), 0, st, W, W2, N, K, perm, (u32x4*)out);
   return hipGetLastError();
 }
 
@@ -56,6 +87,18 @@ hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st
 // remapped so that each XCD receives a contiguous range of tiles (the row
 // tiles and splits of one weight group share an L2).
 constexpr int kWaves = 4;
+
+// With a start/stop event pair, the launch records them from its own dispatch
+// (the kernel's execution time, as a kernel trace reports it).
+template <typename F, typename... A>
+static void launch_timed(F kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                         A... args) {
+  if (e0)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, args...);
+}
+
 
 template <int NF, int MF, int U, int kCK>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ X, int ldx,
@@ -156,6 +199,226 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     }
 }
 
+
+// ---- few-row GEMM with its epilogue, no K split ----------------------------------------
+// For the wide products of a normal step (Q/K/V, gate/up) the whole K range of
+// a 64-feature tile is one workgroup, so its sums are final and the epilogue
+// runs in the kernel: no split-K partials and no epilogue launch.  Same tile
+// as k_gemm_bf16 (4 waves, one 16-row weight group each, activations staged
+// through LDS); the weights of iteration it + 2 are in flight while
+// iteration it is computed (a ring of three register buffers), the
+// activations of it + 1 go to the other half of a double-buffered LDS tile.
+// Loads read clamped addresses, so they are never predicated; K steps past
+// the end are zeroed when stored to LDS and their products add nothing.
+//
+// EPI == kEpiQkv: weights packed kPackRopePair.  Adds the bias, rotates q/k
+// heads (RoPE pairs meet in lanes l and l ^ 32), rounds to T, stores q rows and
+// scatters k/v rows into the cache at row_tok.
+// EPI == kEpiSwiGlu: weights packed kPackGateUp.  out[m][f] = silu(g) * u.
+struct FusedEpi {
+  // Q/K/V
+  const uint16_t* bias;     // [(nh + 2 nkv) * 128] or null
+  const float* rope_cs;     // [pos][64][cos, sin]
+  const int32_t* row_pos;
+  const int32_t* row_tok;
+  int nh, nkv;
+  uint16_t *q, *kc, *vc;
+  long cache_rows;
+  // SwiGLU
+  uint16_t* out;
+  int F;
+};
+
+template <int EPI, int MF, int U>
+__global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restrict__ X, int ldx,
+                                                         const u32x4* __restrict__ Wp, int M, int N,
+                                                         int K, FusedEpi ep) {
+  constexpr int ROWS = 16 * MF;
+  constexpr int PITCH = U * 32 + 8;
+  constexpr int CHUNK16 = ROWS * U * 4;
+  constexpr int PER_T = (CHUNK16 + 255) / 256;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][ROWS * PITCH];
+  const int G = N / (16 * kWaves);
+  int id = blockIdx.x;
+  if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);
+  const int nb = id;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int KT = K >> 5;
+  const int grp = nb * kWaves + wave;  // this wave's 16-row weight group
+  const u32x4* wp = Wp + (long)grp * KT * 64 + lane;
+  f32x4 acc[MF];
+#pragma unroll
+  for (int b = 0; b < MF; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  const int n_it = (KT + U - 1) / U;
+  u32x4 pre[PER_T];
+  u32x4 a0[U], a1[U], a2[U];
+  auto wload = [&](u32x4 (&a)[U], int it) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) a[u] = __builtin_nontemporal_load(wp + (long)min(it * U + u, KT - 1) * 64);
+  };
+  auto xload = [&](int it) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int e = min(tid + i * 256, CHUNK16 - 1);
+      const int r = e / (U * 4), cc = e % (U * 4);
+      const long row = min(r, M - 1);
+      const int kc = min(it * U + cc / 4, KT - 1);
+      pre[i] = *(const u32x4*)(X + row * ldx + kc * 32 + (cc & 3) * 8);
+    }
+  };
+  auto xstore = [&](int buf, int it) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int e = tid + i * 256;
+      if (CHUNK16 % 256 == 0 || e < CHUNK16) {
+        const int r = e / (U * 4), cc = e % (U * 4);
+        const bool ok = r < M && it * U + cc / 4 < KT;
+        *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[i] : zero;
+      }
+    }
+  };
+  auto compute = [&](const u32x4 (&a)[U], int buf) {
+    const uint16_t* xb = xs[buf];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      u32x4 b[MF];
+#pragma unroll
+      for (int j = 0; j < MF; ++j)
+        b[j] = *(const u32x4*)(&xb[(j * 16 + (lane & 15)) * PITCH + u * 32 + (lane >> 4) * 8]);
+#pragma unroll
+      for (int j = 0; j < MF; ++j) acc[j] = mfma16(a[u], b[j], acc[j]);
+    }
+  };
+  auto body = [&](u32x4 (&cur)[U], u32x4 (&ld)[U], int it) {
+    xload(it + 1);
+    wload(ld, it + 2);
+    if (it < n_it) compute(cur, it & 1);
+    xstore((it + 1) & 1, it + 1);
+    __syncthreads();
+  };
+  xload(0);
+  wload(a0, 0);
+  wload(a1, 1);
+  xstore(0, 0);
+  __syncthreads();
+  for (int it = 0; it < n_it; it += 3) {
+    body(a0, a2, it);
+    body(a1, a0, it + 1);
+    body(a2, a1, it + 2);
+  }
+
+  // lane l holds packed rows grp*16 + (l/16)*4 + j (j < 4) of activation rows
+  // j*16 + l%16; packed rows 0..7 of a group pair with rows 8..15 (lane l ^ 32)
+  const int hi = lane >> 5;               // 0: rows 0..7 of the group, 1: rows 8..15
+  const int sub = ((lane >> 4) & 1) * 4;  // first of this lane's 4 rows within its half
+  if constexpr (EPI == kEpiQkv) {
+    const int head = grp >> 3, gi = grp & 7;
+    const int i0 = gi * 8 + sub;          // rotation index of j = 0 (< 64)
+    const int dim0 = hi * 64 + i0;        // this lane's dims dim0 .. dim0 + 3
+    const bool rot = head < ep.nh + ep.nkv;
+    float bias[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bias[j] = ep.bias ? bf2f(ep.bias[head * 128 + dim0 + j]) : 0.f;
+#pragma unroll
+    for (int jf = 0; jf < MF; ++jf) {
+      float x[4], p[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = acc[jf][j] + bias[j];
+        p[j] = __shfl_xor(x[j], 32, 64);
+      }
+      const int m = jf * 16 + (lane & 15);
+      if (m >= M) continue;
+      if (rot) {
+        const float* cs = ep.rope_cs + ((long)ep.row_pos[m] * 64 + i0) * 2;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float c = cs[2 * j], sn = cs[2 * j + 1];
+          x[j] = hi ? x[j] * c + p[j] * sn : x[j] * c - p[j] * sn;
+        }
+      }
+      uint16_t* dst;
+      if (head < ep.nh)
+        dst = ep.q + ((long)m * ep.nh + head) * 128;
+      else if (head < ep.nh + ep.nkv)
+        dst = ep.kc + ((long)(head - ep.nh) * ep.cache_rows + ep.row_tok[m]) * 128;
+      else
+        dst = ep.vc + ((long)(head - ep.nh - ep.nkv) * ep.cache_rows + ep.row_tok[m]) * 128;
+      u32x2 w;
+      w.x = (uint32_t)f2bf(x[0]) | ((uint32_t)f2bf(x[1]) << 16);
+      w.y = (uint32_t)f2bf(x[2]) | ((uint32_t)f2bf(x[3]) << 16);
+      *(u32x2*)(dst + dim0) = w;
+    }
+  } else {
+    const int f0 = grp * 8 + sub;         // this lane's features f0 .. f0 + 3
+#pragma unroll
+    for (int jf = 0; jf < MF; ++jf) {
+      float x[4], p[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = acc[jf][j];
+        p[j] = __shfl_xor(x[j], 32, 64);
+      }
+      const int m = jf * 16 + (lane & 15);
+      if (hi || m >= M) continue;
+      u32x2 w;
+      float y[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) y[j] = x[j] / (1.0f + expf(-x[j])) * p[j];
+      w.x = (uint32_t)f2bf(y[0]) | ((uint32_t)f2bf(y[1]) << 16);
+      w.y = (uint32_t)f2bf(y[2]) | ((uint32_t)f2bf(y[3]) << 16);
+      *(u32x2*)(ep.out + (long)m * ep.F + f0) = w;
+    }
+  }
+}
+
+bool fused_rows_ok(int M, int N, int K) {
+  return M >= 1 && M <= 64 && N % 64 == 0 && K % 32 == 0 && N / 64 >= 192;
+}
+
+template <int EPI, int U>
+static hipError_t launch_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
+                               const FusedEpi& ep, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  if (!fused_rows_ok(M, N, K)) return hipErrorInvalidValue;
+  const dim3 grid(N / 64);
+  const u32x4* W = (const u32x4*)Wp;
+  switch ((M + 15) / 16) {
+    case 1: launch_timed(k_gemm_bf16_fused<EPI, 1, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
+    case 2: launch_timed(k_gemm_bf16_fused<EPI, 2, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
+    case 3: launch_timed(k_gemm_bf16_fused<EPI, 3, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
+    default: launch_timed(k_gemm_bf16_fused<EPI, 4, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
+                               const uint16_t* bias, const float* rope_cs, const int32_t* row_pos,
+                               const int32_t* row_tok, int nh, int nkv, uint16_t* q, uint16_t* kc,
+                               uint16_t* vc, long cache_rows, hipStream_t st, hipEvent_t e0,
+                               hipEvent_t e1) {
+  if (N != (nh + 2 * nkv) * 128) return hipErrorInvalidValue;
+  FusedEpi ep{};
+  ep.bias = bias;
+  ep.rope_cs = rope_cs;
+  ep.row_pos = row_pos;
+  ep.row_tok = row_tok;
+  ep.nh = nh;
+  ep.nkv = nkv;
+  ep.q = q;
+  ep.kc = kc;
+  ep.vc = vc;
+  ep.cache_rows = cache_rows;
+  return launch_fused<kEpiQkv, 8>(X, ldx, Wp, M, N, K, ep, st, e0, e1);
+}
+
+hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, int M, int F, int K,
+                                  uint16_t* out, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  FusedEpi ep{};
+  ep.out = out;
+  ep.F = F;
+  return launch_fused<kEpiSwiGlu, 4>(X, ldx, Wp, M, 2 * F, K, ep, st, e0, e1);
+}
 
 // ---- bf16 GEMM for many rows (refresh steps, the full-sequence path, batches) ----------
 // Same operands and tile order as above, with 128-row activation tiles and
@@ -311,17 +574,6 @@ GemmPlan plan_gemm_bf16(int M, int N, int K) {
   p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
   p.grid = NB * MT * p.splits;
   return p;
-}
-
-// With a start/stop event pair, the launch records them from its own dispatch
-// (the kernel's execution time, as a kernel trace reports it).
-template <typename F, typename... A>
-static void launch_timed(F kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
-                         A... args) {
-  if (e0)
-    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, args...);
-  else
-    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, args...);
 }
 
 template <int NF, int MF>

@@ -21,7 +21,26 @@ struct GemmPlan {
   int grid = 0;
 };
 GemmPlan plan_gemm_bf16(int M, int N, int K);
-hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st);
+// Row orders of packed weights (gemm.hip): plain; RoPE pairs adjacent within
+// each 128-row head (Q/K/V); gate and up interleaved by 8 rows (W2 = up).
+constexpr int kPackPlain = 0, kPackRopePair = 1, kPackGateUp = 2;
+hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st,
+                      int perm = kPackPlain, const uint16_t* W2 = nullptr);
+// Few-row products with their epilogue in the kernel (no K split), for
+// M <= 64 rows when N / 64 >= 192 (fused_rows_ok).  Q/K/V: weights packed
+// kPackRopePair, head_dim 128; writes q [M][nh][128] and the k/v cache rows
+// row_tok of each head.  SwiGLU: weights packed kPackGateUp (N = 2F);
+// writes out [M][F] = silu(gate) * up.
+constexpr int kEpiQkv = 1, kEpiSwiGlu = 2;
+bool fused_rows_ok(int M, int N, int K);
+hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
+                               const uint16_t* bias, const float* rope_cs, const int32_t* row_pos,
+                               const int32_t* row_tok, int nh, int nkv, uint16_t* q, uint16_t* kc,
+                               uint16_t* vc, long cache_rows, hipStream_t st,
+                               hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, int M, int F, int K,
+                                  uint16_t* out, hipStream_t st, hipEvent_t e0 = nullptr,
+                                  hipEvent_t e1 = nullptr);
 // ev_start / ev_stop (optional, both or neither): recorded by the launch itself
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
                      const GemmPlan& p, hipStream_t st, hipEvent_t ev_start = nullptr,

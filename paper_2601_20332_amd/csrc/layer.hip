@@ -106,6 +106,17 @@ hipError_t residual_norm(float* h, const float* C, int S, int M, int H, const T*
 // ---- QKV epilogue: split-K sum, bias, RoPE, q store, K/V cache scatter ------------------
 // Block (r, slot): slot < n_heads is a query head, then n_kv key heads, then
 // n_kv value heads.  Thread i handles the rotation pair (i, i + d/2).
+// bf16 weights are packed with RoPE pairs adjacent (kPackRopePair), so the
+// GEMM's columns of dim i and i + 64 of a head are at group i/8, rows i%8
+// and 8 + i%8; fp32 weights are in plain order.
+template <typename T>
+__device__ __forceinline__ int qkv_col(int head, int i, int d, int partner) {
+  if constexpr (sizeof(T) == 2)
+    return head * 128 + (i >> 3) * 16 + partner * 8 + (i & 7);
+  else
+    return head * d + i + partner * (d >> 1);
+}
+
 template <typename T>
 __global__ void k_qkv_epilogue(const float* __restrict__ C, int S, int M, int N,
                                const T* __restrict__ bias, const float* __restrict__ rope_cs,
@@ -114,9 +125,10 @@ __global__ void k_qkv_epilogue(const float* __restrict__ C, int S, int M, int N,
                                T* __restrict__ q, T* __restrict__ kc, T* __restrict__ vc,
                                long cache_rows) {
   const int r = blockIdx.x, hs = blockIdx.y, i = threadIdx.x, half = d >> 1;
-  const int col = hs * d + i;
+  const int col = hs * d + i;  // feature index of dim i (bias, outputs)
   float x0, x1;
-  split_sum2(C + (long)r * N + col, C + (long)r * N + col + half, (long)M * N, S, x0, x1);
+  split_sum2(C + (long)r * N + qkv_col<T>(hs, i, d, 0), C + (long)r * N + qkv_col<T>(hs, i, d, 1),
+             (long)M * N, S, x0, x1);
   if (bias) {
     x0 += Elem<T>::load(bias + col);
     x1 += Elem<T>::load(bias + col + half);
@@ -154,7 +166,10 @@ hipError_t qkv_epilogue(const float* C, int S, int M, const T* bias, const float
 }
 
 // ---- SwiGLU -----------------------------------------------------------------------------
-// Four consecutive features per thread; F is a multiple of 4.
+// Four consecutive features per thread; F is a multiple of 4 (of 8 for bf16).
+// bf16 weights are packed with gate and up interleaved by 8 rows
+// (kPackGateUp): gate feature f is GEMM column (f/8)*16 + f%8, up feature f
+// is 8 columns later; fp32 weights are gate then up.
 template <typename T>
 __global__ void k_swiglu(const float* __restrict__ C, int S, int M, int F, T* __restrict__ out) {
   const long total = (long)M * F / 4;
@@ -162,9 +177,11 @@ __global__ void k_swiglu(const float* __restrict__ C, int S, int M, int F, T* __
        e += (long)gridDim.x * blockDim.x) {
     const long r = e / (F / 4);
     const int f = (int)(e - r * (F / 4)) * 4;
-    const float* cr = C + r * (2L * F) + f;
+    const int gcol = sizeof(T) == 2 ? (f >> 3) * 16 + (f & 7) : f;
+    const int ucol = sizeof(T) == 2 ? gcol + 8 : F + f;
+    const float* cr = C + r * (2L * F);
     f32x4 g, u;
-    split_sum2((const f32x4*)cr, (const f32x4*)(cr + F), (long)M * F / 2, S, g, u);
+    split_sum2((const f32x4*)(cr + gcol), (const f32x4*)(cr + ucol), (long)M * F / 2, S, g, u);
 #pragma unroll
     for (int q = 0; q < 4; ++q) out[r * F + f + q] = Elem<T>::from_f(g[q] / (1.0f + expf(-g[q])) * u[q]);
   }
@@ -173,7 +190,7 @@ __global__ void k_swiglu(const float* __restrict__ C, int S, int M, int F, T* __
 template <typename T>
 hipError_t swiglu(const float* C, int S, int M, int F, T* out, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (F % 4) return hipErrorInvalidValue;
+  if (F % (sizeof(T) == 2 ? 8 : 4)) return hipErrorInvalidValue;
   const long total = (long)M * F / 4;
   const int blocks = (int)std::min<long>((total + 255) / 256, 8192);
   hipLaunchKernelGGL(k_swiglu<T>, dim3(blocks), dim3(256), 0, st, C, S, M, F, out);
