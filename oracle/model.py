@@ -53,14 +53,27 @@ class KVCache:
         return c
 
 
+# the projection matrices that the FP8-weight variant stores as e4m3
+FP8_MATRICES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "lm_head")
+
+
 class OracleModel:
     """float64 reference model over ``synth.Weights``.
 
     ``cache_budget_bytes`` bounds how many float64 weight tensors stay in
     memory; beyond it tensors are re-read from the seeded generator on use.
+    ``weight_format="fp8"`` (bf16 models only) is the FP8-weight variant: the
+    projection matrices are replaced by their per-row e4m3 quantization
+    (oracle.quant); embeddings, norm gains and biases stay bf16.
     """
 
-    def __init__(self, weights: synth.Weights, cache_budget_bytes: float = 8e9):
+    def __init__(self, weights: synth.Weights, cache_budget_bytes: float = 8e9,
+                 weight_format: str = "bf16"):
+        if weight_format not in ("bf16", "fp8"):
+            raise ValueError("weight_format is 'bf16' or 'fp8'")
+        if weight_format == "fp8" and weights.shape.dtype != synth.DTYPE_BF16:
+            raise ValueError("FP8 weights are a variant of bf16 models")
+        self.weight_format = weight_format
         self.shape = weights.shape
         self.weights = weights
         self.bf16 = self.shape.dtype == synth.DTYPE_BF16
@@ -75,7 +88,11 @@ class OracleModel:
         t = self._cache.get(name)
         if t is not None:
             return t
-        t = self.weights.f32(name).astype(np.float64)
+        if self.weight_format == "fp8" and name.split(".")[-1] in FP8_MATRICES:
+            from .quant import dequantize_rows, quantize_rows
+            t = dequantize_rows(*quantize_rows(self.weights.f32(name)))
+        else:
+            t = self.weights.f32(name).astype(np.float64)
         if self._used + t.nbytes <= self._budget:
             self._cache[name] = t
             self._used += t.nbytes
