@@ -16,8 +16,9 @@ decoding on the same GPU and kernels, the roofline of the dominant kernel
 events on the library's stream; HBM bound), the same for the 128-row-tile GEMM
 of the refresh steps (k_gemm_bf16_big; MFMA bound), adaptive termination at
 <eos> on the same workload (an <eos> id taken from the fixed-length run), the
-buffer-only refresh variant (not the paper's method) and the CPU oracle on a
-bounded sample of the same workload.
+buffer-only refresh variant (not the paper's method), the FP8-weight variant
+(not the paper's precision) and the CPU oracle on a bounded sample of the same
+workload.
 """
 from __future__ import annotations
 
@@ -170,7 +171,9 @@ def roofline_of(model, kernel_class: int, elapsed_ev: float):
     }
 
 
-def upload_model(shape, device):
+def upload_model(shape, device, fp8_too=False):
+    """Packs the seeded weights into the library (and, with fp8_too, a second
+    model of the FP8-weight variant from the same device tensors)."""
     import numpy as np
     import torch
     import synth
@@ -180,15 +183,52 @@ def upload_model(shape, device):
     for _, raw in W.iter_raw(workers=min(16, os.cpu_count() or 4)):
         a = raw.view(np.int16) if raw.dtype == np.uint16 else raw
         ts.append(torch.from_numpy(np.ascontiguousarray(a)).to(device))
-    cfg = wd.model_config(n_layers=shape.n_layers, hidden=shape.hidden, n_heads=shape.n_heads,
-                          n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn=shape.ffn,
-                          vocab=shape.vocab, mask_id=shape.mask_id, dtype=shape.dtype,
-                          qkv_bias=shape.qkv_bias, rms_eps=shape.rms_eps,
-                          rope_theta=shape.rope_theta)
-    m = wd.wd_init_model(cfg, ts, device)
+
+    def cfg(fp8):
+        return wd.model_config(n_layers=shape.n_layers, hidden=shape.hidden,
+                               n_heads=shape.n_heads, n_kv_heads=shape.n_kv_heads,
+                               head_dim=shape.head_dim, ffn=shape.ffn, vocab=shape.vocab,
+                               mask_id=shape.mask_id, dtype=shape.dtype, qkv_bias=shape.qkv_bias,
+                               rms_eps=shape.rms_eps, rope_theta=shape.rope_theta,
+                               weight_fp8=fp8)
+    m = wd.wd_init_model(cfg(False), ts, device)
+    m8 = wd.wd_init_model(cfg(True), ts, device) if fp8_too else None
     del ts
     torch.cuda.empty_cache()
-    return m
+    return (m, m8) if fp8_too else m
+
+
+def fp8_weight_variant(model8, prompts, w, n_steps, fixed_s):
+    """The FP8-weight variant (not the paper's precision): the same windowed
+    generation with e4m3 projection weights, steps/s and the roofline of its
+    few-row GEMMs."""
+    import paper_2601_20332_amd as wd
+    import torch
+    win = w.window
+    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
+    generation(model8, prompts, w.gen_len, wc, n_steps)  # warm
+    torch.cuda.synchronize()
+    reps = 2
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        generation(model8, prompts, w.gen_len, wc, n_steps)
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / reps
+    wd.wd_profile_enable(model8, True)
+    t1 = time.perf_counter()
+    generation(model8, prompts, w.gen_len, wc, n_steps)
+    torch.cuda.synchronize()
+    roof = roofline_of(model8, wd.WD_PROF_GEMM_ROWS, time.perf_counter() - t1)
+    wd.wd_profile_enable(model8, False)
+    if roof:
+        roof["traffic"] = None  # the counter runs cover the bf16 kernels only
+    return {
+        "variant": "fp8 (e4m3) projection weights with per-row scales (not the paper's precision)",
+        "steps_per_s": round(n_steps / t, 3),
+        "ms_per_generation": round(t * 1e3, 2),
+        "speedup_vs_bf16": round(fixed_s / t, 3),
+        "roofline": roof,
+    }
 
 
 def generation(model, prompts, G, wc, n_steps, full=False):
@@ -403,7 +443,11 @@ def main():
     device = "cuda:0"
     torch.cuda.set_device(0)
     t0 = time.time()
-    model = upload_model(w.model, device)
+    want_fp8 = not args.no_variants and len(synth.prompt_lengths(w)) == 1
+    if want_fp8:
+        model, model8 = upload_model(w.model, device, fp8_too=True)
+    else:
+        model, model8 = upload_model(w.model, device), None
     log(f"[bench] {args.workload}: weights generated and packed in {time.time() - t0:.1f}s")
     prompts = synth.prompts(w.model, synth.prompt_lengths(w))
     win = w.window
@@ -452,10 +496,14 @@ def main():
         t_full = time.perf_counter() - tf
         full_speedup = round(t_full / (elapsed / args.steps), 3)
         log(f"[bench] full-sequence generation {t_full:.3f}s")
-    variant = None
+    variant = fp8 = None
     if not args.no_variants and len(prompts) == 1:
         variant = buffer_refresh_variant(model, prompts, w, n_steps, elapsed / args.steps)
         log(f"[bench] buffer-only refresh variant: {variant}")
+    if model8 is not None:
+        fp8 = fp8_weight_variant(model8, prompts, w, n_steps, elapsed / args.steps)
+        log(f"[bench] fp8-weight variant: {fp8}")
+        model8.free()
     adaptive = None
     if not args.no_eos:
         adaptive = adaptive_termination(model, prompts, w, n_steps, elapsed / args.steps)
@@ -503,6 +551,7 @@ def main():
         "roofline_tiled_gemm": roofline_tiled,
         "adaptive_termination": adaptive,
         "buffer_refresh_variant": variant,
+        "fp8_weight_variant": fp8,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -64,6 +64,13 @@ typedef struct {
   int32_t qkv_bias;  /* 0 or 1 */
   float rms_eps;
   float rope_theta;
+  int32_t weight_fp8; /* 0 (default): weights as given.  1: the FP8-weight variant (not the
+                         paper's precision; bf16 models only): wd_init_model stores every
+                         projection matrix (Q/K/V, output, gate/up, down, LM head) as e4m3
+                         codes with one float32 scale per output row, s = max |w| / 448, code =
+                         nearest e4m3 value to w / s (ties to even); embeddings, norm gains
+                         and biases stay bf16.  The GEMMs decode to bf16 and scale their fp32
+                         sums. */
 } wd_model_config;
 
 /* Window settings (Sec. 4.2, Sec. 4.3): the internal window holds n_active
@@ -247,6 +254,18 @@ wd_status wd_debug_kv(const wd_seq* s, int32_t layer, int32_t b, float* k, float
                       int32_t capacity, int32_t* ctx_len);
 
 void wd_free_seq(wd_seq* s); /* NULL is a no-op; synchronizes the stream */
+
+/* Tests only.  The values the GEMMs use for output row `row` of weight
+ * tensor `tensor` (an index into the wd_init_model order; projection
+ * matrices only: wq, wk, wv, wo, wg, wu, wd, lm_head), read back from the
+ * packed device buffer and decoded on the host: `values` receives the row's
+ * in_features weights in their original column order (bf16 values, or the
+ * e4m3 values before scaling with weight_fp8) and *scale the row's fp8
+ * scale (1 without weight_fp8).  Synchronizes.  WD_ERR_INVALID_ARG for an
+ * index that is not a projection matrix or a row out of range;
+ * WD_ERR_UNSUPPORTED for fp32 models. */
+wd_status wd_debug_weight_row(const wd_model* m, int32_t tensor, int32_t row, float* values,
+                              float* scale);
 
 /* ---- kernel timing ------------------------------------------------------------- */
 

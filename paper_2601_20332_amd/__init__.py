@@ -30,7 +30,7 @@ EXPORTED = ["wd_weight_count", "wd_weight_shape", "wd_model_bytes", "wd_init_mod
             "wd_free_model", "wd_seq_bytes", "wd_prefill_prompt", "wd_slide_window",
             "wd_refresh_buffer", "wd_step", "wd_full_step", "wd_get_state", "wd_debug_logits",
             "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error", "wd_profile_enable",
-            "wd_profile_read", "wd_seq_ends"]
+            "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row"]
 
 
 class WdError(RuntimeError):
@@ -45,7 +45,8 @@ class ModelConfig(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("mask_id", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("qkv_bias", ctypes.c_int32),
-                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float),
+                ("weight_fp8", ctypes.c_int32)]
 
 
 class WindowConfig(ctypes.Structure):
@@ -72,7 +73,7 @@ def _load() -> ctypes.CDLL:
     except ImportError:
         pass
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2601_20332_amd.build` "
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2601_20332_amd/build.py` "
                           "(or __graft_entry__.build())")
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.c_void_p
@@ -95,6 +96,8 @@ def _load() -> ctypes.CDLL:
         "wd_full_step": (i32, [P, ctypes.POINTER(StepOut)]),
         "wd_get_state": (i32, [P, pi32, ctypes.POINTER(ctypes.c_uint8), pi32]),
         "wd_seq_ends": (i32, [P, pi32]),
+        "wd_debug_weight_row": (i32, [P, i32, i32, ctypes.POINTER(ctypes.c_float),
+                                      ctypes.POINTER(ctypes.c_float)]),
         "wd_debug_logits": (i32, [P, ctypes.POINTER(ctypes.c_float), pi32, i32, pi32]),
         "wd_debug_kv": (i32, [P, i32, i32, ctypes.POINTER(ctypes.c_float),
                               ctypes.POINTER(ctypes.c_float), i32, pi32]),
@@ -129,10 +132,11 @@ def _f32p(a: np.ndarray):
 
 
 def model_config(*, n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab, mask_id, dtype,
-                 qkv_bias, rms_eps, rope_theta) -> ModelConfig:
+                 qkv_bias, rms_eps, rope_theta, weight_fp8: bool = False) -> ModelConfig:
+    """weight_fp8 selects the FP8-weight variant (bf16 models; not the paper's precision)."""
     return ModelConfig(n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab, mask_id,
                        WD_DTYPE_BF16 if dtype in ("bf16", WD_DTYPE_BF16) else WD_DTYPE_F32,
-                       int(bool(qkv_bias)), rms_eps, rope_theta)
+                       int(bool(qkv_bias)), rms_eps, rope_theta, int(bool(weight_fp8)))
 
 
 def window_config(n_active, n_buffer, refresh_every, unmask_per_step,
@@ -296,6 +300,14 @@ def wd_get_state(gen: Generation):
         out_d.append(dec[o:o + n].astype(bool))
         o += n
     return out_t, out_d, t.value
+
+
+def wd_debug_weight_row(model: Model, tensor: int, row: int, in_features: int):
+    """(values [in_features] as the GEMMs use them before scaling, fp8 row scale)."""
+    vals = np.empty(in_features, np.float32)
+    sc = ctypes.c_float()
+    _check(lib.wd_debug_weight_row(model.handle, int(tensor), int(row), _f32p(vals), ctypes.byref(sc)))
+    return vals, sc.value
 
 
 def wd_seq_ends(gen: Generation) -> np.ndarray:

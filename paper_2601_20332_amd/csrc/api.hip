@@ -91,6 +91,14 @@ bool cfg_valid(const wd_model_config* c, std::string* why) {
     *why = "mask_id outside [0, vocab)";
     return false;
   }
+  if (c->weight_fp8 != 0 && c->weight_fp8 != 1) {
+    *why = "weight_fp8 must be 0 or 1";
+    return false;
+  }
+  if (c->weight_fp8 && c->dtype != WD_DTYPE_BF16) {
+    *why = "fp8 weights are a variant of bf16 models";
+    return false;
+  }
   if (c->qkv_bias != 0 && c->qkv_bias != 1) {
     *why = "qkv_bias must be 0 or 1";
     return false;
@@ -104,30 +112,32 @@ bool cfg_valid(const wd_model_config* c, std::string* why) {
 
 struct TensorSpec {
   long rows, cols;
+  std::string name;  // as in the wd_init_model order: emb, layers.<l>.wq, ..., lm_head
 };
 
 std::vector<TensorSpec> tensor_specs(const wd_model_config& c) {
   const long H = c.hidden, Q = (long)c.n_heads * c.head_dim, KV = (long)c.n_kv_heads * c.head_dim;
   std::vector<TensorSpec> v;
-  v.push_back({c.vocab, H});
+  v.push_back({c.vocab, H, "emb"});
   for (int l = 0; l < c.n_layers; ++l) {
-    v.push_back({H, 1});
-    v.push_back({Q, H});
-    v.push_back({KV, H});
-    v.push_back({KV, H});
+    const std::string p = "layers." + std::to_string(l) + ".";
+    v.push_back({H, 1, p + "attn_norm"});
+    v.push_back({Q, H, p + "wq"});
+    v.push_back({KV, H, p + "wk"});
+    v.push_back({KV, H, p + "wv"});
     if (c.qkv_bias) {
-      v.push_back({Q, 1});
-      v.push_back({KV, 1});
-      v.push_back({KV, 1});
+      v.push_back({Q, 1, p + "bq"});
+      v.push_back({KV, 1, p + "bk"});
+      v.push_back({KV, 1, p + "bv"});
     }
-    v.push_back({H, Q});
-    v.push_back({H, 1});
-    v.push_back({c.ffn, H});
-    v.push_back({c.ffn, H});
-    v.push_back({H, c.ffn});
+    v.push_back({H, Q, p + "wo"});
+    v.push_back({H, 1, p + "ffn_norm"});
+    v.push_back({c.ffn, H, p + "wg"});
+    v.push_back({c.ffn, H, p + "wu"});
+    v.push_back({H, c.ffn, p + "wd"});
   }
-  v.push_back({H, 1});
-  v.push_back({c.vocab, H});
+  v.push_back({H, 1, "final_norm"});
+  v.push_back({c.vocab, H, "lm_head"});
   return v;
 }
 
@@ -163,6 +173,14 @@ struct Counts {
     ++j;
   }
 };
+
+// Host decode of an e4m3 code (sign, 4-bit exponent with bias 7, 3-bit
+// mantissa; exponent 0 holds m * 2^-9) for wd_debug_weight_row.
+float e4m3_to_float(uint8_t c) {
+  const int e = (c >> 3) & 15, m = c & 7;
+  const float mag = e == 0 ? std::ldexp((float)m, -9) : std::ldexp(1.f + m / 8.f, e - 7);
+  return (c & 0x80) ? -mag : mag;
+}
 
 // Exact host copy of one sequence's schedule under adaptive termination
 // (Sec. 4.2): the live end, the decoded flags, the phase's window and its
@@ -234,6 +252,8 @@ struct LayerW {
   const void* ffn_norm;
   const void* wgu;
   const void* wd;
+  // fp8 row scales of the packed matrices (NULL with bf16 / fp32 weights)
+  const float *sqkv, *so, *sgu, *sd;
 };
 
 struct wd_model {
@@ -245,6 +265,7 @@ struct wd_model {
   const void* emb;
   const void* final_norm;
   const void* lm;
+  const float* slm = nullptr;  // fp8 row scales of the LM head
   std::vector<LayerW> layers;
   int live_seqs = 0;
   // kernel timing (wd_profile_enable)
@@ -260,9 +281,10 @@ namespace {
 // Byte layout of the packed weight buffer; the same walk sizes and fills it.
 struct ModelLayout {
   size_t total = 0;
-  size_t emb, final_norm, lm;
+  size_t emb, final_norm, lm, slm = 0;
   struct L {
     size_t attn_norm, wqkv, bqkv, wo, ffn_norm, wgu, wd;
+    size_t sqkv = 0, so = 0, sgu = 0, sd = 0;  // fp8 row scales
   };
   std::vector<L> layers;
 };
@@ -278,20 +300,30 @@ ModelLayout model_layout(const wd_model_config& c) {
     o += align256(bytes);
     return at;
   };
+  // projection matrices: bf16 fragments (2 bytes per weight), or e4m3 codes
+  // (1 byte) plus a float32 scale per output row
+  const bool w8 = c.weight_fp8 != 0;
+  const size_t ew = w8 ? 1 : e;
+  auto scales = [&](size_t rows) { return w8 ? take(rows * 4) : (size_t)0; };
   m.emb = take((size_t)c.vocab * H * e);
   for (int l = 0; l < c.n_layers; ++l) {
     ModelLayout::L L;
     L.attn_norm = take(H * e);
-    L.wqkv = take((Q + 2 * KV) * H * e);
+    L.wqkv = take((Q + 2 * KV) * H * ew);
+    L.sqkv = scales(Q + 2 * KV);
     L.bqkv = c.qkv_bias ? take((Q + 2 * KV) * e) : 0;
-    L.wo = take(H * Q * e);
+    L.wo = take(H * Q * ew);
+    L.so = scales(H);
     L.ffn_norm = take(H * e);
-    L.wgu = take(2 * F * H * e);
-    L.wd = take(H * F * e);
+    L.wgu = take(2 * F * H * ew);
+    L.sgu = scales(2 * F);
+    L.wd = take(H * F * ew);
+    L.sd = scales(H);
     m.layers.push_back(L);
   }
   m.final_norm = take(H * e);
-  m.lm = take((size_t)c.vocab * H * e);
+  m.lm = take((size_t)c.vocab * H * ew);
+  m.slm = scales(c.vocab);
   m.total = o;
   return m;
 }
@@ -300,8 +332,12 @@ ModelLayout model_layout(const wd_model_config& c) {
 // bf16 weights are packed into MFMA fragments (rows reordered by perm, W2 =
 // the up half of kPackGateUp); fp32 weights are copied as they are.
 wd_status put_matrix(const wd_model& m, const void* src, long N, long K, char* dst,
-                     int perm = wd::kPackPlain, const void* src2 = nullptr) {
-  if (m.cfg.dtype == WD_DTYPE_BF16) {
+                     int perm = wd::kPackPlain, const void* src2 = nullptr,
+                     float* scale = nullptr) {
+  if (m.cfg.weight_fp8) {
+    WD_HIP(wd::pack_fp8((const uint16_t*)src, (int)N, (int)K, dst, scale, m.stream, perm,
+                        (const uint16_t*)src2));
+  } else if (m.cfg.dtype == WD_DTYPE_BF16) {
     WD_HIP(wd::pack_frags((const uint16_t*)src, (int)N, (int)K, dst, m.stream, perm,
                           (const uint16_t*)src2));
   } else {
@@ -380,6 +416,8 @@ wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, 
   const long H = cfg->hidden, Q = (long)cfg->n_heads * cfg->head_dim,
              KV = (long)cfg->n_kv_heads * cfg->head_dim, F = cfg->ffn;
   const size_t e = m->esz;
+  const bool w8 = cfg->weight_fp8 != 0;
+  const size_t ew = w8 ? 1 : e;  // bytes per packed projection weight
   auto fail_free = [&](wd_status s) {
     delete m;
     return s;
@@ -401,25 +439,38 @@ wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, 
     const void* wk = weights[wi++];
     const void* wv = weights[wi++];
     const int rp = wd::kPackRopePair;
-    if ((st = put_matrix(*m, wq, Q, H, base + L.wqkv, rp)) != WD_OK) return fail_free(st);
-    if ((st = put_matrix(*m, wk, KV, H, base + L.wqkv + Q * H * e, rp)) != WD_OK) return fail_free(st);
-    if ((st = put_matrix(*m, wv, KV, H, base + L.wqkv + (Q + KV) * H * e, rp)) != WD_OK)
+    float* sq = w8 ? (float*)(base + L.sqkv) : nullptr;
+    if ((st = put_matrix(*m, wq, Q, H, base + L.wqkv, rp, nullptr, sq)) != WD_OK) return fail_free(st);
+    if ((st = put_matrix(*m, wk, KV, H, base + L.wqkv + Q * H * ew, rp, nullptr, w8 ? sq + Q : nullptr)) !=
+        WD_OK)
       return fail_free(st);
+    if ((st = put_matrix(*m, wv, KV, H, base + L.wqkv + (Q + KV) * H * ew, rp, nullptr,
+                         w8 ? sq + Q + KV : nullptr)) != WD_OK)
+      return fail_free(st);
+    w.sqkv = sq;
     if (cfg->qkv_bias) {
       if ((st = copy(weights[wi++], Q * e, base + L.bqkv)) != WD_OK) return fail_free(st);
       if ((st = copy(weights[wi++], KV * e, base + L.bqkv + Q * e)) != WD_OK) return fail_free(st);
       if ((st = copy(weights[wi++], KV * e, base + L.bqkv + (Q + KV) * e)) != WD_OK) return fail_free(st);
       w.bqkv = base + L.bqkv;
     }
-    if ((st = put_matrix(*m, weights[wi++], H, Q, base + L.wo)) != WD_OK) return fail_free(st);
+    w.so = w8 ? (float*)(base + L.so) : nullptr;
+    if ((st = put_matrix(*m, weights[wi++], H, Q, base + L.wo, wd::kPackPlain, nullptr,
+                         (float*)w.so)) != WD_OK)
+      return fail_free(st);
     if ((st = copy(weights[wi++], H * e, base + L.ffn_norm)) != WD_OK) return fail_free(st);
     {
       const void* wg = weights[wi++];
       const void* wu = weights[wi++];
-      if ((st = put_matrix(*m, wg, 2 * F, H, base + L.wgu, wd::kPackGateUp, wu)) != WD_OK)
+      w.sgu = w8 ? (float*)(base + L.sgu) : nullptr;
+      if ((st = put_matrix(*m, wg, 2 * F, H, base + L.wgu, wd::kPackGateUp, wu, (float*)w.sgu)) !=
+          WD_OK)
         return fail_free(st);
     }
-    if ((st = put_matrix(*m, weights[wi++], H, F, base + L.wd)) != WD_OK) return fail_free(st);
+    w.sd = w8 ? (float*)(base + L.sd) : nullptr;
+    if ((st = put_matrix(*m, weights[wi++], H, F, base + L.wd, wd::kPackPlain, nullptr,
+                         (float*)w.sd)) != WD_OK)
+      return fail_free(st);
     w.attn_norm = base + L.attn_norm;
     w.wqkv = base + L.wqkv;
     w.wo = base + L.wo;
@@ -430,7 +481,10 @@ wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, 
   }
   if ((st = copy(weights[wi++], H * e, base + lay.final_norm)) != WD_OK) return fail_free(st);
   m->final_norm = base + lay.final_norm;
-  if ((st = put_matrix(*m, weights[wi++], cfg->vocab, H, base + lay.lm)) != WD_OK) return fail_free(st);
+  m->slm = w8 ? (float*)(base + lay.slm) : nullptr;
+  if ((st = put_matrix(*m, weights[wi++], cfg->vocab, H, base + lay.lm, wd::kPackPlain, nullptr,
+                       (float*)m->slm)) != WD_OK)
+    return fail_free(st);
   m->lm = base + lay.lm;
   if (hipStreamSynchronize(m->stream) != hipSuccess) {
     delete m;
@@ -444,6 +498,78 @@ void wd_free_model(wd_model* m) {
   if (!m) return;
   for (hipEvent_t e : m->ev) (void)hipEventDestroy(e);
   delete m;
+}
+
+wd_status wd_debug_weight_row(const wd_model* m, int32_t tensor, int32_t row, float* values,
+                              float* scale) {
+  if (!m || !values || !scale) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  const wd_model_config& c = m->cfg;
+  if (c.dtype != WD_DTYPE_BF16) return fail(WD_ERR_UNSUPPORTED, "fp32 weights are not packed");
+  const auto specs = tensor_specs(c);
+  if (tensor < 0 || tensor >= (int32_t)specs.size())
+    return fail(WD_ERR_INVALID_ARG, "tensor %d out of range", tensor);
+  const std::string name = specs[tensor].name;
+  const std::string leaf = name.substr(name.rfind('.') + 1);
+  const long H = c.hidden, Q = (long)c.n_heads * c.head_dim, KV = (long)c.n_kv_heads * c.head_dim,
+             F = c.ffn;
+  int layer = -1;
+  if (name.compare(0, 7, "layers.") == 0) layer = std::stoi(name.substr(7));
+  // the packed matrix holding the tensor, its K, and the packed row of `row`
+  const char* base = nullptr;
+  const float* sc = nullptr;
+  long K = H, rows = 0, prow = 0;
+  auto rope_row = [](long r) {  // kPackRopePair: dim d of head h
+    const long h = r >> 7, d = r & 127;
+    return h * 128 + ((d & 63) >> 3) * 16 + (d >= 64 ? 8 : 0) + (d & 7);
+  };
+  const bool w8 = c.weight_fp8 != 0;
+  const size_t ew = w8 ? 1 : 2;
+  if (layer >= 0) {
+    const LayerW& w = m->layers[layer];
+    if (leaf == "wq" || leaf == "wk" || leaf == "wv") {
+      const long off = leaf == "wq" ? 0 : leaf == "wk" ? Q : Q + KV;
+      rows = leaf == "wq" ? Q : KV;
+      if (row < 0 || row >= rows) return fail(WD_ERR_INVALID_ARG, "row %d out of range", row);
+      base = (const char*)w.wqkv + off * H * ew;
+      sc = w.sqkv ? w.sqkv + off : nullptr;
+      prow = rope_row(row);
+    } else if (leaf == "wo") {
+      rows = H, K = Q, base = (const char*)w.wo, sc = w.so, prow = row;
+    } else if (leaf == "wg" || leaf == "wu") {
+      rows = F, base = (const char*)w.wgu, sc = w.sgu;
+      prow = (row >> 3) * 16 + (leaf == "wu" ? 8 : 0) + (row & 7);
+    } else if (leaf == "wd") {
+      rows = H, K = F, base = (const char*)w.wd, sc = w.sd, prow = row;
+    }
+  } else if (leaf == "lm_head") {
+    rows = c.vocab, base = (const char*)m->lm, sc = m->slm, prow = row;
+  }
+  if (!base) return fail(WD_ERR_INVALID_ARG, "tensor %d (%s) is not a projection matrix", tensor,
+                         name.c_str());
+  if (row < 0 || row >= rows) return fail(WD_ERR_INVALID_ARG, "row %d out of range", row);
+  // one 16-row group is contiguous: K/32 bf16 fragments, or K/64 fp8 fragments, of 1 KB
+  const long g = prow >> 4, r = prow & 15, frags = w8 ? K / 64 : K / 32;
+  std::vector<uint8_t> buf((size_t)frags * 1024);
+  WD_HIP(hipStreamSynchronize(m->stream));
+  WD_HIP(hipMemcpy(buf.data(), base + (size_t)g * frags * 1024, buf.size(), hipMemcpyDeviceToHost));
+  for (long f = 0; f < frags; ++f)
+    for (int q = 0; q < 4; ++q) {
+      const uint8_t* lane = buf.data() + (size_t)f * 1024 + (size_t)(q * 16 + r) * 16;
+      for (int j = 0; j < 8; ++j) {
+        if (w8) {
+          values[f * 64 + q * 8 + j] = e4m3_to_float(lane[j]);
+          values[f * 64 + 32 + q * 8 + j] = e4m3_to_float(lane[8 + j]);
+        } else {
+          uint16_t h;
+          memcpy(&h, lane + 2 * j, 2);
+          const uint32_t u = (uint32_t)h << 16;
+          memcpy(&values[f * 32 + q * 8 + j], &u, 4);
+        }
+      }
+    }
+  *scale = 1.f;
+  if (sc) WD_HIP(hipMemcpy(scale, sc + prow, 4, hipMemcpyDeviceToHost));
+  return WD_OK;
 }
 
 wd_status wd_profile_enable(wd_model* m, int32_t enable) {
@@ -678,7 +804,9 @@ wd_status profile_begin(wd_model& m, hipEvent_t* e0, hipEvent_t* e1) {
 
 wd_status profile_end(wd_model& m, int kind, int M, int N, int K, size_t esz) {
   if (!m.profile) return WD_OK;
-  m.rec_bytes.push_back((double)N * K * esz + (double)M * K * esz + (double)M * N * 4);
+  // weights: esz bytes each, or one byte plus a float32 scale per row with fp8
+  const double wbytes = m.cfg.weight_fp8 ? (double)N * K + 4.0 * N : (double)N * K * esz;
+  m.rec_bytes.push_back(wbytes + (double)M * K * esz + (double)M * N * 4);
   m.rec_flops.push_back(2.0 * M * N * K);
   m.rec_kind.push_back(kind);
   m.n_rec++;
@@ -686,11 +814,12 @@ wd_status profile_end(wd_model& m, int kind, int M, int N, int K, size_t esz) {
 }
 
 template <typename T>
-wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
-                      int max_splits, int* splits, int* kind, hipEvent_t e0, hipEvent_t e1) {
+wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, const float* wsc, float* C,
+                      int M, int N, int K, int max_splits, int* splits, int* kind, hipEvent_t e0,
+                      hipEvent_t e1) {
   const wd_model& m = *s->m;
   if (m.cfg.dtype == WD_DTYPE_BF16) {
-    wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K);
+    wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K, wsc != nullptr);
     if (p.splits > max_splits) {
       p.splits = 1;
       p.ks_per_split = K / 32;
@@ -698,7 +827,7 @@ wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, float* C, i
     }
     if ((size_t)p.splits * M * N > s->C_floats && C == s->C)
       return fail(WD_ERR_DEVICE, "internal: partial buffer too small");
-    WD_HIP(wd::gemm_bf16((const uint16_t*)X, ldx, W, C, M, N, K, p, m.stream, e0, e1));
+    WD_HIP(wd::gemm_bf16((const uint16_t*)X, ldx, W, C, M, N, K, p, m.stream, e0, e1, wsc));
     *splits = p.splits;
     *kind = p.mf == 8 ? WD_PROF_GEMM_TILED : WD_PROF_GEMM_ROWS;
   } else {
@@ -710,13 +839,13 @@ wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, float* C, i
 }
 
 template <typename T>
-wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, float* C, int M, int N, int K,
-               int max_splits, int* splits) {
+wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, const float* wsc, float* C, int M,
+               int N, int K, int max_splits, int* splits) {
   wd_model& m = *s->m;
   int kind = WD_PROF_ALL;
   hipEvent_t e0, e1;
   WD_TRY(profile_begin(m, &e0, &e1));
-  WD_TRY(gemm_launch<T>(s, X, ldx, W, C, M, N, K, max_splits, splits, &kind, e0, e1));
+  WD_TRY(gemm_launch<T>(s, X, ldx, W, wsc, C, M, N, K, max_splits, splits, &kind, e0, e1));
   return profile_end(m, kind, M, N, K, m.esz);
 }
 
@@ -752,10 +881,10 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
       WD_HIP(wd::gemm_bf16_qkv_fused((const uint16_t*)a, H, w.wqkv, M, m.qkv_n, H,
                                      (const uint16_t*)w.bqkv, s->rope, s->row_pos, s->row_tok,
                                      c.n_heads, c.n_kv_heads, (uint16_t*)q, (uint16_t*)kc,
-                                     (uint16_t*)vc, s->T, st, e0, e1));
+                                     (uint16_t*)vc, s->T, st, e0, e1, w.sqkv));
       WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, m.qkv_n, H, m.esz));
     } else {
-      WD_TRY(gemm<T>(s, a, H, w.wqkv, s->C, M, m.qkv_n, H, 1 << 20, &S));
+      WD_TRY(gemm<T>(s, a, H, w.wqkv, w.sqkv, s->C, M, m.qkv_n, H, 1 << 20, &S));
       WD_HIP(wd::qkv_epilogue<T>(s->C, S, M, (const T*)w.bqkv, s->rope, s->row_pos, s->row_tok,
                                  c.n_heads, c.n_kv_heads, c.head_dim, q, kc, vc, s->T, st));
     }
@@ -768,19 +897,19 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
                                (float*)o, s->row_seq, M, r.g, c.n_heads, c.n_kv_heads, c.head_dim,
                                st));
     }
-    WD_TRY(gemm<T>(s, o, Q, w.wo, s->C, M, H, Q, 1 << 20, &S));
+    WD_TRY(gemm<T>(s, o, Q, w.wo, w.so, s->C, M, H, Q, 1 << 20, &S));
     WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)w.ffn_norm, c.rms_eps, a, nullptr, st));
     if (fused_rows(m, M, 2 * F, H)) {
       hipEvent_t e0, e1;
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_swiglu_fused((const uint16_t*)a, H, w.wgu, M, F, H, (uint16_t*)sw, st,
-                                        e0, e1));
+                                        e0, e1, w.sgu));
       WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, 2 * F, H, m.esz));
     } else {
-      WD_TRY(gemm<T>(s, a, H, w.wgu, s->C, M, 2 * F, H, 1 << 20, &S));
+      WD_TRY(gemm<T>(s, a, H, w.wgu, w.sgu, s->C, M, 2 * F, H, 1 << 20, &S));
       WD_HIP(wd::swiglu<T>(s->C, S, M, F, sw, st));
     }
-    WD_TRY(gemm<T>(s, sw, F, w.wd, s->C, M, H, F, 1 << 20, &S));
+    WD_TRY(gemm<T>(s, sw, F, w.wd, w.sd, s->C, M, H, F, 1 << 20, &S));
     if (l + 1 < c.n_layers) {
       WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)m.layers[l + 1].attn_norm,
                                   c.rms_eps, a, nullptr, st));
@@ -820,11 +949,11 @@ wd_status decide(wd_seq* s, int n_act) {
   const int n = s->B * n_act;
   int S;
   if (c.dtype == WD_DTYPE_BF16)
-    WD_TRY(gemm<uint16_t>(s, (const uint16_t*)s->a_act, c.hidden, m.lm, s->logits, n, c.vocab,
-                          c.hidden, 1, &S));
+    WD_TRY(gemm<uint16_t>(s, (const uint16_t*)s->a_act, c.hidden, m.lm, m.slm, s->logits, n,
+                          c.vocab, c.hidden, 1, &S));
   else
-    WD_TRY(gemm<float>(s, (const float*)s->a_act, c.hidden, m.lm, s->logits, n, c.vocab, c.hidden,
-                       1, &S));
+    WD_TRY(gemm<float>(s, (const float*)s->a_act, c.hidden, m.lm, nullptr, s->logits, n, c.vocab,
+                       c.hidden, 1, &S));
   WD_HIP(wd::confidence(s->logits, n, c.vocab, c.mask_id, s->act_tok, s->act_conf, s->conf_scratch,
                         m.stream));
   const WdStepGeom g = base_geom(s);

@@ -75,6 +75,114 @@ hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st
   return hipGetLastError();
 }
 
+// ---- FP8 (e4m3) weights: per-row scales, packing, decode ----------------------------
+// The FP8-weight variant stores each projection matrix as e4m3 codes with one
+// float32 scale per output row: s_n = max_k |W[n][k]| / 448 (1 for a zero
+// row), code = the e4m3 value nearest to W[n][k] / s_n (float32 quotient,
+// ties to the even code, saturating at 448).  A packed fp8 fragment (nt, kt2)
+// holds packed rows nt*16..+15 and K columns kt2*64..+63: lane l holds row
+// nt*16 + l%16, K columns kt2*64 + (l/16)*8 .. +7 (bytes 0-7) and
+// kt2*64 + 32 + (l/16)*8 .. +7 (bytes 8-15), i.e. the A operands of K steps
+// 2 kt2 and 2 kt2 + 1 once decoded to bf16 (e4m3 values are exact in bf16).
+// The GEMMs multiply each output feature's fp32 sum by its scale.
+__device__ __forceinline__ uint32_t e4m3_code(float x) {
+  const uint32_t sign = (__float_as_uint(x) >> 31) << 7;
+  const float a = fabsf(x);
+  if (!(a < 448.f)) return sign | 0x7Eu;
+  if (a < 0x1p-6f) return sign | (uint32_t)rintf(a * 512.f);  // m * 2^-9; m = 8 is 2^-6
+  int e;
+  const float mant = frexpf(a, &e) * 2.f;                       // a = mant * 2^(e-1)
+  float q = rintf((mant - 1.f) * 8.f);
+  int E = e - 1 + 7;
+  if (q == 8.f) {
+    q = 0.f;
+    ++E;
+  }
+  const uint32_t code = min((uint32_t)(E << 3) | (uint32_t)q, 0x7Eu);
+  return sign | code;
+}
+
+__global__ __launch_bounds__(256) void k_row_scale(const uint16_t* __restrict__ W,
+                                                   const uint16_t* __restrict__ W2, int N, int K,
+                                                   int perm, float* __restrict__ scale) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  int which;
+  const long src = packed_source_row(perm, row, N, which);
+  const uint16_t* w = (which ? W2 : W) + src * K;
+  float m = 0.f;
+  for (int k = threadIdx.x; k < K; k += blockDim.x) m = fmaxf(m, fabsf(bf2f(w[k])));
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float a = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    scale[row] = a > 0.f ? __fdiv_rn(a, 448.f) : 1.f;
+  }
+}
+
+__global__ void k_pack_fp8(const uint16_t* __restrict__ W, const uint16_t* __restrict__ W2, int N,
+                           int K, int perm, const float* __restrict__ scale,
+                           u32x4* __restrict__ out) {
+  const int KT2 = K >> 6;
+  const long total = (long)(N >> 4) * KT2 * 64;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long)gridDim.x * blockDim.x) {
+    const int lane = (int)(i & 63);
+    const long f = i >> 6;
+    const int kt2 = (int)(f % KT2);
+    const long nt = f / KT2;
+    const long prow = nt * 16 + (lane & 15);
+    int which;
+    const long row = packed_source_row(perm, prow, N, which);
+    const uint16_t* w = (which ? W2 : W) + row * K + kt2 * 64 + (lane >> 4) * 8;
+    const float s = scale[prow];
+    uint32_t b[16];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      b[j] = e4m3_code(__fdiv_rn(bf2f(w[j]), s));
+      b[8 + j] = e4m3_code(__fdiv_rn(bf2f(w[32 + j]), s));
+    }
+    u32x4 v;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      v[q] = b[4 * q] | (b[4 * q + 1] << 8) | (b[4 * q + 2] << 16) | (b[4 * q + 3] << 24);
+    out[i] = v;
+  }
+}
+
+hipError_t pack_fp8(const uint16_t* W, int N, int K, void* out, float* scale, hipStream_t st,
+                    int perm, const uint16_t* W2) {
+  if (N % 16 || K % 64) return hipErrorInvalidValue;
+  if (perm == kPackRopePair && N % 128) return hipErrorInvalidValue;
+  if (perm == kPackGateUp && !W2) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_row_scale, dim3(N), dim3(256), 0, st, W, W2, N, K, perm, scale);
+  const long total = (long)(N / 16) * (K / 64) * 64;
+  const int blocks = (int)std::min<long>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_pack_fp8, dim3(blocks), dim3(256), 0, st, W, W2, N, K, perm, scale,
+                     (u32x4*)out);
+  return hipGetLastError();
+}
+
+// 4 e4m3 codes -> 4 bf16 (2 words): hardware conversion to f32, which is exact,
+// then the top 16 bits of each value.
+__device__ __forceinline__ u32x2 bf16x4_of_fp8x4(uint32_t w) {
+  const auto a = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  const auto b = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+  u32x2 r;
+  r.x = (__float_as_uint(a[0]) >> 16) | (__float_as_uint(a[1]) & 0xFFFF0000u);
+  r.y = (__float_as_uint(b[0]) >> 16) | (__float_as_uint(b[1]) & 0xFFFF0000u);
+  return r;
+}
+
+// A packed fp8 fragment -> the bf16 A operands of its two K steps.
+__device__ __forceinline__ void fp8_frag_to_bf16(const u32x4 raw, u32x4& k0, u32x4& k1) {
+  const u32x2 p = bf16x4_of_fp8x4(raw.x), q = bf16x4_of_fp8x4(raw.y);
+  const u32x2 r = bf16x4_of_fp8x4(raw.z), t = bf16x4_of_fp8x4(raw.w);
+  k0 = u32x4{p.x, p.y, q.x, q.y};
+  k1 = u32x4{r.x, r.y, t.x, t.y};
+}
+
 // ---- bf16 weight-streaming GEMM ----------------------------------------------------
 // Workgroup = 4 waves; wave w owns NF 16-row weight groups (the workgroup
 // covers 64*NF output features), all four waves walk the same K range.  The
@@ -100,11 +208,14 @@ static void launch_timed(F kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hip
 }
 
 
-template <int NF, int MF, int U, int kCK>
+// W8: fp8 weights (packed fp8 fragments, one per two K steps) with per-row
+// scales wsc; the fp32 results are multiplied by the scale of their feature.
+template <int NF, int MF, int U, int kCK, bool W8>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ X, int ldx,
                                                    const u32x4* __restrict__ Wp,
                                                    float* __restrict__ C, int M, int N, int K,
-                                                   int NB, int MT, int S, int ks_per_split) {
+                                                   int NB, int MT, int S, int ks_per_split,
+                                                   const float* __restrict__ wsc) {
   constexpr int ROWS = 16 * MF;
   constexpr int PITCH = kCK * 32 + 8;   // bf16 per LDS row; the 16-byte pad spreads banks
   constexpr int CHUNK16 = ROWS * kCK * 4;
@@ -123,9 +234,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
   const int kt1 = min(KT, kt0 + ks_per_split);
   const int m0 = mt * ROWS;
   const int f0 = (nb * kWaves + wave) * NF;
+  const int frags = W8 ? KT / 2 : KT;  // packed fragments per 16-row group
   const u32x4* wp[NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) wp[f] = Wp + ((long)(f0 + f) * KT) * 64 + lane;
+  for (int f = 0; f < NF; ++f) wp[f] = Wp + ((long)(f0 + f) * frags) * 64 + lane;
   f32x4 acc[NF][MF];
 #pragma unroll
   for (int a = 0; a < NF; ++a)
@@ -167,11 +279,27 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     const int nk = min(kCK, kt1 - kbase);
     for (int k = 0; k < nk; k += U) {
       u32x4 a[U][NF];
+      if constexpr (W8) {
+        // K steps come in pairs (split and chunk starts are even)
+        u32x4 raw[U / 2][NF];
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+        for (int u = 0; u < U; u += 2)
 #pragma unroll
-        for (int f = 0; f < NF; ++f)
-          a[u][f] = (k + u < nk) ? __builtin_nontemporal_load(wp[f] + (long)(kbase + k + u) * 64) : zero;
+          for (int f = 0; f < NF; ++f)
+            raw[u / 2][f] = (k + u < nk)
+                                ? __builtin_nontemporal_load(wp[f] + (long)((kbase + k + u) >> 1) * 64)
+                                : zero;
+#pragma unroll
+        for (int u = 0; u < U; u += 2)
+#pragma unroll
+          for (int f = 0; f < NF; ++f) fp8_frag_to_bf16(raw[u / 2][f], a[u][f], a[u + 1][f]);
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int f = 0; f < NF; ++f)
+            a[u][f] = (k + u < nk) ? __builtin_nontemporal_load(wp[f] + (long)(kbase + k + u) * 64) : zero;
+      }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         u32x4 b[MF];
@@ -191,12 +319,15 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     }
   }
 #pragma unroll
-  for (int i = 0; i < NF; ++i)
+  for (int i = 0; i < NF; ++i) {
+    const int n0 = (f0 + i) * 16 + (lane >> 4) * 4;
+    const f32x4 sc = W8 ? *(const f32x4*)(wsc + n0) : f32x4{1.f, 1.f, 1.f, 1.f};
 #pragma unroll
     for (int j = 0; j < MF; ++j) {
       const int m = m0 + j * 16 + (lane & 15);
-      if (m < M) *(f32x4*)(C + ((long)s * M + m) * N + (f0 + i) * 16 + (lane >> 4) * 4) = acc[i][j];
+      if (m < M) *(f32x4*)(C + ((long)s * M + m) * N + n0) = W8 ? acc[i][j] * sc : acc[i][j];
     }
+  }
 }
 
 
@@ -229,10 +360,11 @@ struct FusedEpi {
   int F;
 };
 
-template <int EPI, int MF, int U>
+template <int EPI, int MF, int U, bool W8>
 __global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restrict__ X, int ldx,
                                                          const u32x4* __restrict__ Wp, int M, int N,
-                                                         int K, FusedEpi ep) {
+                                                         int K, FusedEpi ep,
+                                                         const float* __restrict__ wsc) {
   constexpr int ROWS = 16 * MF;
   constexpr int PITCH = U * 32 + 8;
   constexpr int CHUNK16 = ROWS * U * 4;
@@ -245,17 +377,21 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restr
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int KT = K >> 5;
   const int grp = nb * kWaves + wave;  // this wave's 16-row weight group
-  const u32x4* wp = Wp + (long)grp * KT * 64 + lane;
+  // W8: the ring holds raw fp8 fragments (one per two K steps), decoded when used
+  constexpr int UW = W8 ? U / 2 : U;
+  const int frags = W8 ? KT / 2 : KT;
+  const u32x4* wp = Wp + (long)grp * frags * 64 + lane;
   f32x4 acc[MF];
 #pragma unroll
   for (int b = 0; b < MF; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
   const u32x4 zero = {0u, 0u, 0u, 0u};
   const int n_it = (KT + U - 1) / U;
   u32x4 pre[PER_T];
-  u32x4 a0[U], a1[U], a2[U];
-  auto wload = [&](u32x4 (&a)[U], int it) {
+  u32x4 a0[UW], a1[UW], a2[UW];
+  auto wload = [&](u32x4 (&a)[UW], int it) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) a[u] = __builtin_nontemporal_load(wp + (long)min(it * U + u, KT - 1) * 64);
+    for (int u = 0; u < UW; ++u)
+      a[u] = __builtin_nontemporal_load(wp + (long)min(it * UW + u, frags - 1) * 64);
   };
   auto xload = [&](int it) {
 #pragma unroll
@@ -278,19 +414,29 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restr
       }
     }
   };
-  auto compute = [&](const u32x4 (&a)[U], int buf) {
+  auto compute = [&](const u32x4 (&a)[UW], int buf) {
     const uint16_t* xb = xs[buf];
+    constexpr int PAIR = W8 ? 2 : 1;  // K steps per weight register of the ring
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      u32x4 b[MF];
+    for (int uw = 0; uw < UW; ++uw) {
+      u32x4 w[PAIR];
+      if constexpr (W8)
+        fp8_frag_to_bf16(a[uw], w[0], w[1]);
+      else
+        w[0] = a[uw];
 #pragma unroll
-      for (int j = 0; j < MF; ++j)
-        b[j] = *(const u32x4*)(&xb[(j * 16 + (lane & 15)) * PITCH + u * 32 + (lane >> 4) * 8]);
+      for (int h = 0; h < PAIR; ++h) {
+        const int u = uw * PAIR + h;
+        u32x4 b[MF];
 #pragma unroll
-      for (int j = 0; j < MF; ++j) acc[j] = mfma16(a[u], b[j], acc[j]);
+        for (int j = 0; j < MF; ++j)
+          b[j] = *(const u32x4*)(&xb[(j * 16 + (lane & 15)) * PITCH + u * 32 + (lane >> 4) * 8]);
+#pragma unroll
+        for (int j = 0; j < MF; ++j) acc[j] = mfma16(w[h], b[j], acc[j]);
+      }
     }
   };
-  auto body = [&](u32x4 (&cur)[U], u32x4 (&ld)[U], int it) {
+  auto body = [&](u32x4 (&cur)[UW], u32x4 (&ld)[UW], int it) {
     xload(it + 1);
     wload(ld, it + 2);
     if (it < n_it) compute(cur, it & 1);
@@ -312,6 +458,11 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restr
   // j*16 + l%16; packed rows 0..7 of a group pair with rows 8..15 (lane l ^ 32)
   const int hi = lane >> 5;               // 0: rows 0..7 of the group, 1: rows 8..15
   const int sub = ((lane >> 4) & 1) * 4;  // first of this lane's 4 rows within its half
+  if constexpr (W8) {
+    const f32x4 sc = *(const f32x4*)(wsc + grp * 16 + (lane >> 4) * 4);
+#pragma unroll
+    for (int jf = 0; jf < MF; ++jf) acc[jf] *= sc;
+  }
   if constexpr (EPI == kEpiQkv) {
     const int head = grp >> 3, gi = grp & 7;
     const int i0 = gi * 8 + sub;          // rotation index of j = 0 (< 64)
@@ -377,18 +528,29 @@ bool fused_rows_ok(int M, int N, int K) {
   return M >= 1 && M <= 64 && N % 64 == 0 && K % 32 == 0 && N / 64 >= 192;
 }
 
+template <int EPI, int U, bool W8>
+static void launch_fused_mf(dim3 grid, int M, const uint16_t* X, int ldx, const u32x4* W, int N,
+                            int K, const FusedEpi& ep, const float* wsc, hipStream_t st,
+                            hipEvent_t e0, hipEvent_t e1) {
+  switch ((M + 15) / 16) {
+    case 1: launch_timed(k_gemm_bf16_fused<EPI, 1, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 2: launch_timed(k_gemm_bf16_fused<EPI, 2, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 3: launch_timed(k_gemm_bf16_fused<EPI, 3, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    default: launch_timed(k_gemm_bf16_fused<EPI, 4, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+  }
+}
+
 template <int EPI, int U>
 static hipError_t launch_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
-                               const FusedEpi& ep, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-  if (!fused_rows_ok(M, N, K)) return hipErrorInvalidValue;
+                               const FusedEpi& ep, const float* wsc, hipStream_t st, hipEvent_t e0,
+                               hipEvent_t e1) {
+  if (!fused_rows_ok(M, N, K) || (wsc && K % 64)) return hipErrorInvalidValue;
   const dim3 grid(N / 64);
   const u32x4* W = (const u32x4*)Wp;
-  switch ((M + 15) / 16) {
-    case 1: launch_timed(k_gemm_bf16_fused<EPI, 1, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
-    case 2: launch_timed(k_gemm_bf16_fused<EPI, 2, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
-    case 3: launch_timed(k_gemm_bf16_fused<EPI, 3, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
-    default: launch_timed(k_gemm_bf16_fused<EPI, 4, U>, grid, st, e0, e1, X, ldx, W, M, N, K, ep); break;
-  }
+  if (wsc)
+    launch_fused_mf<EPI, U, true>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
+  else
+    launch_fused_mf<EPI, U, false>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
   return hipGetLastError();
 }
 
@@ -396,7 +558,7 @@ hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M
                                const uint16_t* bias, const float* rope_cs, const int32_t* row_pos,
                                const int32_t* row_tok, int nh, int nkv, uint16_t* q, uint16_t* kc,
                                uint16_t* vc, long cache_rows, hipStream_t st, hipEvent_t e0,
-                               hipEvent_t e1) {
+                               hipEvent_t e1, const float* wsc) {
   if (N != (nh + 2 * nkv) * 128) return hipErrorInvalidValue;
   FusedEpi ep{};
   ep.bias = bias;
@@ -409,15 +571,16 @@ hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M
   ep.kc = kc;
   ep.vc = vc;
   ep.cache_rows = cache_rows;
-  return launch_fused<kEpiQkv, 8>(X, ldx, Wp, M, N, K, ep, st, e0, e1);
+  return launch_fused<kEpiQkv, 8>(X, ldx, Wp, M, N, K, ep, wsc, st, e0, e1);
 }
 
 hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, int M, int F, int K,
-                                  uint16_t* out, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+                                  uint16_t* out, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                                  const float* wsc) {
   FusedEpi ep{};
   ep.out = out;
   ep.F = F;
-  return launch_fused<kEpiSwiGlu, 4>(X, ldx, Wp, M, 2 * F, K, ep, st, e0, e1);
+  return launch_fused<kEpiSwiGlu, 4>(X, ldx, Wp, M, 2 * F, K, ep, wsc, st, e0, e1);
 }
 
 // ---- bf16 GEMM for many rows (refresh steps, the full-sequence path, batches) ----------
@@ -427,12 +590,13 @@ hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, in
 // two iterations (8 K steps) ahead through a ring of three register buffers,
 // the next activation chunk one iteration ahead into the other half of a
 // double-buffered LDS tile; one barrier per iteration.
-template <int NF>
+template <int NF, bool W8>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __restrict__ X, int ldx,
                                                           const u32x4* __restrict__ Wp,
                                                           float* __restrict__ C, int M, int N,
                                                           int K, int NB, int MT, int S,
-                                                          int ks_per_split) {
+                                                          int ks_per_split,
+                                                          const float* __restrict__ wsc) {
   constexpr int MF = 8, U = 4;
   constexpr int ROWS = 16 * MF;
   constexpr int PITCH = U * 32 + 8;
@@ -452,9 +616,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
   const int kt1 = min(KT, kt0 + ks_per_split);
   const int m0 = mt * ROWS;
   const int f0 = (nb * kWaves + wave) * NF;
+  // W8: the ring holds raw fp8 fragments (one per two K steps), decoded when used
+  constexpr int UW = W8 ? U / 2 : U;
+  const int frags = W8 ? KT / 2 : KT;
   const u32x4* wp[NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) wp[f] = Wp + ((long)(f0 + f) * KT) * 64 + lane;
+  for (int f = 0; f < NF; ++f) wp[f] = Wp + ((long)(f0 + f) * frags) * 64 + lane;
   f32x4 acc[NF][MF];
 #pragma unroll
   for (int a = 0; a < NF; ++a)
@@ -463,18 +630,19 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
   const u32x4 zero = {0u, 0u, 0u, 0u};
   const int n_it = (kt1 - kt0 + U - 1) / U;
   u32x4 pre[PER_T];
-  u32x4 a0[U][NF], a1[U][NF], a2[U][NF];
+  u32x4 a0[UW][NF], a1[UW][NF], a2[UW][NF];
 
   // Loads are branch-free and never waited on early: an out-of-range K step
   // reads the weights of the last valid step (finite values, multiplied by
   // the zero activations stored for that step), and out-of-range activation
   // elements read a clamped address and are zeroed only when they are
   // stored to LDS.
-  auto wload = [&](u32x4 (&a)[U][NF], int it) {
+  auto wload = [&](u32x4 (&a)[UW][NF], int it) {
     const int kb = kt0 + it * U;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kk = min(kb + u, kt1 - 1);
+    for (int u = 0; u < UW; ++u) {
+      // W8: split starts and U are even, so fragment (kb + 2u) / 2 holds steps kb + 2u, + 1
+      const int kk = W8 ? min((kb >> 1) + u, (kt1 >> 1) - 1) : min(kb + u, kt1 - 1);
 #pragma unroll
       for (int f = 0; f < NF; ++f) a[u][f] = __builtin_nontemporal_load(wp[f] + (long)kk * 64);
     }
@@ -500,24 +668,37 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
       *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[i] : zero;
     }
   };
-  auto compute = [&](const u32x4 (&a)[U][NF], int buf) {
+  auto compute = [&](const u32x4 (&a)[UW][NF], int buf) {
     const uint16_t* xb = xs[buf];
+    constexpr int PAIR = W8 ? 2 : 1;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      u32x4 b[MF];
+    for (int uw = 0; uw < UW; ++uw) {
+      u32x4 w[PAIR][NF];
 #pragma unroll
-      for (int j = 0; j < MF; ++j)
-        b[j] = *(const u32x4*)(&xb[(j * 16 + (lane & 15)) * PITCH + u * 32 + (lane >> 4) * 8]);
+      for (int i = 0; i < NF; ++i) {
+        if constexpr (W8)
+          fp8_frag_to_bf16(a[uw][i], w[0][i], w[1][i]);
+        else
+          w[0][i] = a[uw][i];
+      }
 #pragma unroll
-      for (int j = 0; j < MF; ++j)
+      for (int h = 0; h < PAIR; ++h) {
+        const int u = uw * PAIR + h;
+        u32x4 b[MF];
 #pragma unroll
-        for (int i = 0; i < NF; ++i) acc[i][j] = mfma16(a[u][i], b[j], acc[i][j]);
+        for (int j = 0; j < MF; ++j)
+          b[j] = *(const u32x4*)(&xb[(j * 16 + (lane & 15)) * PITCH + u * 32 + (lane >> 4) * 8]);
+#pragma unroll
+        for (int j = 0; j < MF; ++j)
+#pragma unroll
+          for (int i = 0; i < NF; ++i) acc[i][j] = mfma16(w[h][i], b[j], acc[i][j]);
+      }
     }
   };
   // iteration it: weights of it come from `cur`, weights of it + 2 go to `ld`
   // The activation loads go first: the load counter is in order, so waiting
   // for them before the LDS store must not also wait for the weight prefetch.
-  auto body = [&](u32x4 (&cur)[U][NF], u32x4 (&ld)[U][NF], int it) {
+  auto body = [&](u32x4 (&cur)[UW][NF], u32x4 (&ld)[UW][NF], int it) {
     const bool more = it + 1 < n_it;
     if (more) xload(it + 1);
     if (it + 2 < n_it) wload(ld, it + 2);
@@ -537,12 +718,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
     if (it + 2 < n_it) body(a2, a1, it + 2);
   }
 #pragma unroll
-  for (int i = 0; i < NF; ++i)
+  for (int i = 0; i < NF; ++i) {
+    const int n0 = (f0 + i) * 16 + (lane >> 4) * 4;
+    const f32x4 sc = W8 ? *(const f32x4*)(wsc + n0) : f32x4{1.f, 1.f, 1.f, 1.f};
 #pragma unroll
     for (int j = 0; j < MF; ++j) {
       const int m = m0 + j * 16 + (lane & 15);
-      if (m < M) *(f32x4*)(C + ((long)s * M + m) * N + (f0 + i) * 16 + (lane >> 4) * 4) = acc[i][j];
+      if (m < M) *(f32x4*)(C + ((long)s * M + m) * N + n0) = W8 ? acc[i][j] * sc : acc[i][j];
     }
+  }
 }
 
 // Launch shape, from the measured behaviour of the kernel on MI355X.
@@ -553,7 +737,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
 // full-sequence path, batches): 128-row tiles, 2 weight groups per wave,
 // software-pipelined, K splits until 256 workgroups run (split-K partials
 // cost rows*N*4 bytes each).
-GemmPlan plan_gemm_bf16(int M, int N, int K) {
+GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8) {
   GemmPlan p;
   const int KT = K / 32;
   if (M <= 64) {
@@ -571,36 +755,43 @@ GemmPlan plan_gemm_bf16(int M, int N, int K) {
   int S = 1;
   while ((long)NB * MT * S < target && KT / (2 * S) >= p.ck) S *= 2;
   p.ks_per_split = (KT + S - 1) / S;
+  if (w8) p.ks_per_split += p.ks_per_split & 1;  // fp8 fragments hold K steps in pairs
   p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
   p.grid = NB * MT * p.splits;
   return p;
 }
 
-template <int NF, int MF>
+template <int NF, int MF, bool W8>
 static void launch_mf(dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, const uint16_t* X,
                       int ldx, const void* Wp, float* C, int M, int N, int K, int NB, int MT,
-                      int S, int ks) {
+                      int S, int ks, const float* wsc) {
   if constexpr (MF == 8) {
-    launch_timed(k_gemm_bf16_big<NF>, grid, st, e0, e1, X, ldx, (const u32x4*)Wp, C, M, N, K, NB,
-                 MT, S, ks);
+    launch_timed(k_gemm_bf16_big<NF, W8>, grid, st, e0, e1, X, ldx, (const u32x4*)Wp, C, M, N, K,
+                 NB, MT, S, ks, wsc);
   } else {
-    launch_timed(k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4, 8>, grid, st, e0, e1, X, ldx,
-                 (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks);
+    launch_timed(k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4, 8, W8>, grid, st, e0, e1, X, ldx,
+                 (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks, wsc);
   }
 }
 
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
-                     const GemmPlan& p, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                     const GemmPlan& p, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
+                     const float* wsc) {
   if (M <= 0) return hipSuccess;
   const int NB = N / (16 * kWaves * p.nf);
   const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
   if (NB * MT * p.splits != p.grid || N % (16 * kWaves * p.nf) || K % 32) return hipErrorInvalidValue;
+  if (wsc && (K % 64 || p.ks_per_split % 2)) return hipErrorInvalidValue;
   const dim3 grid(p.grid);
   bool launched = false;
 #define WD_GEMM_CASE(NF, MF)                                                                  \
   if (p.nf == NF && p.mf == MF) {                                                             \
-    launch_mf<NF, MF>(grid, st, ev_start, ev_stop, X, ldx, Wp, C, M, N, K, NB, MT, p.splits, \
-                      p.ks_per_split);                                                        \
+    if (wsc)                                                                                  \
+      launch_mf<NF, MF, true>(grid, st, ev_start, ev_stop, X, ldx, Wp, C, M, N, K, NB, MT,    \
+                              p.splits, p.ks_per_split, wsc);                                 \
+    else                                                                                      \
+      launch_mf<NF, MF, false>(grid, st, ev_start, ev_stop, X, ldx, Wp, C, M, N, K, NB, MT,   \
+                               p.splits, p.ks_per_split, wsc);                                \
     launched = true;                                                                          \
   }
   WD_GEMM_CASE(1, 1) WD_GEMM_CASE(1, 2) WD_GEMM_CASE(1, 3) WD_GEMM_CASE(1, 4)

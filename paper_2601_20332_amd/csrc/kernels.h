@@ -20,12 +20,16 @@ struct GemmPlan {
   int ks_per_split = 0;  // 32-wide K steps per split
   int grid = 0;
 };
-GemmPlan plan_gemm_bf16(int M, int N, int K);
+GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8 = false);
 // Row orders of packed weights (gemm.hip): plain; RoPE pairs adjacent within
 // each 128-row head (Q/K/V); gate and up interleaved by 8 rows (W2 = up).
 constexpr int kPackPlain = 0, kPackRopePair = 1, kPackGateUp = 2;
 hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st,
                       int perm = kPackPlain, const uint16_t* W2 = nullptr);
+// FP8-weight variant: per-row scales (in packed row order) and e4m3 fragments
+// of 16 rows x 64 K columns (N x K bytes); K a multiple of 64.
+hipError_t pack_fp8(const uint16_t* W, int N, int K, void* out, float* scale, hipStream_t st,
+                    int perm = kPackPlain, const uint16_t* W2 = nullptr);
 // Few-row products with their epilogue in the kernel (no K split), for
 // M <= 64 rows when N / 64 >= 192 (fused_rows_ok).  Q/K/V: weights packed
 // kPackRopePair, head_dim 128; writes q [M][nh][128] and the k/v cache rows
@@ -37,14 +41,16 @@ hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M
                                const uint16_t* bias, const float* rope_cs, const int32_t* row_pos,
                                const int32_t* row_tok, int nh, int nkv, uint16_t* q, uint16_t* kc,
                                uint16_t* vc, long cache_rows, hipStream_t st,
-                               hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+                               hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr,
+                               const float* wsc = nullptr);
 hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, int M, int F, int K,
                                   uint16_t* out, hipStream_t st, hipEvent_t e0 = nullptr,
-                                  hipEvent_t e1 = nullptr);
-// ev_start / ev_stop (optional, both or neither): recorded by the launch itself
+                                  hipEvent_t e1 = nullptr, const float* wsc = nullptr);
+// ev_start / ev_stop (optional, both or neither): recorded by the launch itself.
+// wsc: per-row scales of fp8 weights (packed by pack_fp8), null for bf16.
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
                      const GemmPlan& p, hipStream_t st, hipEvent_t ev_start = nullptr,
-                     hipEvent_t ev_stop = nullptr);
+                     hipEvent_t ev_stop = nullptr, const float* wsc = nullptr);
 hipError_t gemm_f32(const float* X, int ldx, const float* W, float* C, int M, int N, int K,
                     hipStream_t st, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 

@@ -36,24 +36,25 @@ def log(*a):
     sys.stdout.flush()
 
 
-def cfg_of(shape: synth.ModelShape):
+def cfg_of(shape: synth.ModelShape, weight_fp8: bool = False):
     import paper_2601_20332_amd as wd
     return wd.model_config(n_layers=shape.n_layers, hidden=shape.hidden, n_heads=shape.n_heads,
                            n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn=shape.ffn,
                            vocab=shape.vocab, mask_id=shape.mask_id, dtype=shape.dtype,
                            qkv_bias=shape.qkv_bias, rms_eps=shape.rms_eps,
-                           rope_theta=shape.rope_theta)
+                           rope_theta=shape.rope_theta, weight_fp8=weight_fp8)
 
 
-def gpu_model(W: synth.Weights, device="cuda"):
-    """Uploads the seeded weights and packs them (the originals are dropped)."""
+def gpu_model(W: synth.Weights, device="cuda", weight_fp8: bool = False):
+    """Uploads the seeded weights and packs them (the originals are dropped);
+    weight_fp8 selects the FP8-weight variant (the library quantizes them)."""
     import torch
     import paper_2601_20332_amd as wd
     ts = []
     for _, raw in W.iter_raw(workers=8):
         a = raw.view(np.int16) if raw.dtype == np.uint16 else raw
         ts.append(torch.from_numpy(np.ascontiguousarray(a)).to(device))
-    m = wd.wd_init_model(cfg_of(W.shape), ts, device)
+    m = wd.wd_init_model(cfg_of(W.shape, weight_fp8), ts, device)
     del ts
     return m
 
