@@ -768,8 +768,14 @@ static void launch_mf(dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, c
   if constexpr (MF == 8) {
     launch_timed(k_gemm_bf16_big<NF, W8>, grid, st, e0, e1, X, ldx, (const u32x4*)Wp, C, M, N, K,
                  NB, MT, S, ks, wsc);
+  } else if constexpr (W8) {
+    // fp8 fragments carry two K steps; with one weight group per wave, twice
+    // the steps per batch (the same bytes in flight) measured faster, with
+    // two groups (LM head) the bf16 batch did
+    launch_timed(k_gemm_bf16<NF, MF, NF == 1 ? 16 : 4, NF == 1 ? 16 : 8, true>, grid, st, e0, e1,
+                 X, ldx, (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks, wsc);
   } else {
-    launch_timed(k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4, 8, W8>, grid, st, e0, e1, X, ldx,
+    launch_timed(k_gemm_bf16<NF, MF, NF == 1 ? 8 : 4, 8, false>, grid, st, e0, e1, X, ldx,
                  (const u32x4*)Wp, C, M, N, K, NB, MT, S, ks, wsc);
   }
 }
