@@ -238,11 +238,21 @@ wd_status wd_seq_ends(const wd_seq* s, int32_t* ends);
  * 1 = decoded) may be NULL. */
 wd_status wd_get_state(const wd_seq* s, int32_t* tokens, uint8_t* decoded, int32_t* t);
 
+/* on != 0: every later step also stores its active-row logits for
+ * wd_debug_logits.  Off by default: with bf16 and at most 64 active rows the
+ * LM head reduces each 64-entry vocabulary tile to the confidence inputs
+ * (maximum, its lowest id, sum of exponentials; Section 3, the confidence
+ * rule) inside the GEMM and the logits never reach memory.  The decisions
+ * are the same either way.  For tests. */
+wd_status wd_debug_keep_logits(wd_seq* s, int32_t on);
+
 /* Synchronizes, then copies the last step's active-row logits (fp32,
  * [n_rows, vocab], sequence after sequence, active positions in increasing
  * order) and, when `positions` is not NULL, those rows' positions; *n_rows
  * receives the row count.  `capacity` is the number of rows the caller's
- * arrays hold (WD_ERR_OUT_OF_MEMORY if too small).  For tests. */
+ * arrays hold (WD_ERR_OUT_OF_MEMORY if too small).  WD_ERR_STATE when the
+ * last step kept no logits (none yet, or the fused LM head ran without
+ * wd_debug_keep_logits).  For tests. */
 wd_status wd_debug_logits(const wd_seq* s, float* logits, int32_t* positions, int32_t capacity,
                           int32_t* n_rows);
 

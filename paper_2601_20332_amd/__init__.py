@@ -30,7 +30,7 @@ EXPORTED = ["wd_weight_count", "wd_weight_shape", "wd_model_bytes", "wd_init_mod
             "wd_free_model", "wd_seq_bytes", "wd_prefill_prompt", "wd_slide_window",
             "wd_refresh_buffer", "wd_step", "wd_full_step", "wd_get_state", "wd_debug_logits",
             "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error", "wd_profile_enable",
-            "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row"]
+            "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row", "wd_debug_keep_logits"]
 
 
 class WdError(RuntimeError):
@@ -98,6 +98,7 @@ def _load() -> ctypes.CDLL:
         "wd_seq_ends": (i32, [P, pi32]),
         "wd_debug_weight_row": (i32, [P, i32, i32, ctypes.POINTER(ctypes.c_float),
                                       ctypes.POINTER(ctypes.c_float)]),
+        "wd_debug_keep_logits": (i32, [P, i32]),
         "wd_debug_logits": (i32, [P, ctypes.POINTER(ctypes.c_float), pi32, i32, pi32]),
         "wd_debug_kv": (i32, [P, i32, i32, ctypes.POINTER(ctypes.c_float),
                               ctypes.POINTER(ctypes.c_float), i32, pi32]),
@@ -315,6 +316,10 @@ def wd_seq_ends(gen: Generation) -> np.ndarray:
     out = np.empty(gen.batch, np.int32)
     _check(lib.wd_seq_ends(gen.handle, _i32p(out)))
     return out
+
+
+def wd_debug_keep_logits(gen: Generation, on: bool = True) -> None:
+    _check(lib.wd_debug_keep_logits(gen.handle, int(bool(on))))
 
 
 def wd_debug_logits(gen: Generation):

@@ -621,6 +621,9 @@ struct wd_seq {
   bool refreshed = false;
   int mode = 0;  // 0 = not started, 1 = windowed, 2 = full sequence
   int last_nA = 0;
+  // logits of the last step's active rows: written only on request when the
+  // LM head reduces its tiles to the confidence inputs itself
+  bool keep_logits = false, logits_valid = false;
   // adaptive termination
   int eos_id = -1;
   std::vector<Track> tr;
@@ -705,7 +708,9 @@ SeqLayout seq_layout(const wd_model& m, const wd_window_config& w, int B, long T
                                                                            w.refresh_every));
   s.attn_part_floats = 16L * rows_normal * c.n_heads * (c.head_dim + 2);
   s.attn_part = take(s.attn_part_floats * 4);
-  s.conf_scratch = take((size_t)3 * s.A_max * wd::kConfChunks * 4);
+  // confidence partials: kConfChunks per row, or one per 64-entry vocabulary
+  // tile when the LM head reduces them itself
+  s.conf_scratch = take((size_t)3 * s.A_max * std::max<long>(wd::kConfChunks, c.vocab / 64) * 4);
   s.total = o;
   return s;
 }
@@ -802,11 +807,14 @@ wd_status profile_begin(wd_model& m, hipEvent_t* e0, hipEvent_t* e1) {
   return WD_OK;
 }
 
-wd_status profile_end(wd_model& m, int kind, int M, int N, int K, size_t esz) {
+// out_bytes: what the launch writes (fp32 M x N when negative).
+wd_status profile_end(wd_model& m, int kind, int M, int N, int K, size_t esz,
+                      double out_bytes = -1) {
   if (!m.profile) return WD_OK;
   // weights: esz bytes each, or one byte plus a float32 scale per row with fp8
   const double wbytes = m.cfg.weight_fp8 ? (double)N * K + 4.0 * N : (double)N * K * esz;
-  m.rec_bytes.push_back(wbytes + (double)M * K * esz + (double)M * N * 4);
+  if (out_bytes < 0) out_bytes = (double)M * N * 4;
+  m.rec_bytes.push_back(wbytes + (double)M * K * esz + out_bytes);
   m.rec_flops.push_back(2.0 * M * N * K);
   m.rec_kind.push_back(kind);
   m.n_rec++;
@@ -882,7 +890,8 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
                                      (const uint16_t*)w.bqkv, s->rope, s->row_pos, s->row_tok,
                                      c.n_heads, c.n_kv_heads, (uint16_t*)q, (uint16_t*)kc,
                                      (uint16_t*)vc, s->T, st, e0, e1, w.sqkv));
-      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, m.qkv_n, H, m.esz));
+      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, m.qkv_n, H, m.esz,
+                         (double)M * m.qkv_n * m.esz));
     } else {
       WD_TRY(gemm<T>(s, a, H, w.wqkv, w.sqkv, s->C, M, m.qkv_n, H, 1 << 20, &S));
       WD_HIP(wd::qkv_epilogue<T>(s->C, S, M, (const T*)w.bqkv, s->rope, s->row_pos, s->row_tok,
@@ -904,7 +913,7 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_swiglu_fused((const uint16_t*)a, H, w.wgu, M, F, H, (uint16_t*)sw, st,
                                         e0, e1, w.sgu));
-      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, 2 * F, H, m.esz));
+      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, 2 * F, H, m.esz, (double)M * F * m.esz));
     } else {
       WD_TRY(gemm<T>(s, a, H, w.wgu, w.sgu, s->C, M, 2 * F, H, 1 << 20, &S));
       WD_HIP(wd::swiglu<T>(s->C, S, M, F, sw, st));
@@ -948,14 +957,33 @@ wd_status decide(wd_seq* s, int n_act) {
   const wd_model_config& c = m.cfg;
   const int n = s->B * n_act;
   int S;
-  if (c.dtype == WD_DTYPE_BF16)
-    WD_TRY(gemm<uint16_t>(s, (const uint16_t*)s->a_act, c.hidden, m.lm, m.slm, s->logits, n,
-                          c.vocab, c.hidden, 1, &S));
-  else
-    WD_TRY(gemm<float>(s, (const float*)s->a_act, c.hidden, m.lm, nullptr, s->logits, n, c.vocab,
-                       c.hidden, 1, &S));
-  WD_HIP(wd::confidence(s->logits, n, c.vocab, c.mask_id, s->act_tok, s->act_conf, s->conf_scratch,
-                        m.stream));
+  if (fused_rows(m, n, c.vocab, c.hidden)) {
+    // the LM head reduces each 64-entry vocabulary tile to the confidence
+    // inputs itself; the logits reach memory only when asked for
+    const int n_tiles = c.vocab / 64;
+    float* pmax = s->conf_scratch;
+    int* pidx = (int*)(pmax + (size_t)n * n_tiles);
+    float* psum = pmax + 2 * (size_t)n * n_tiles;
+    hipEvent_t e0, e1;
+    WD_TRY(profile_begin(m_mut(s), &e0, &e1));
+    WD_HIP(wd::gemm_bf16_lmhead_conf((const uint16_t*)s->a_act, c.hidden, m.lm, n, c.vocab,
+                                     c.hidden, c.mask_id, s->keep_logits ? s->logits : nullptr,
+                                     pmax, pidx, psum, m.stream, e0, e1, m.slm));
+    WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, n, c.vocab, c.hidden, m.esz,
+                       12.0 * n * n_tiles + (s->keep_logits ? 4.0 * n * c.vocab : 0.0)));
+    WD_HIP(wd::confidence_tiles(pmax, pidx, psum, n, n_tiles, s->act_tok, s->act_conf, m.stream));
+    s->logits_valid = s->keep_logits;
+  } else {
+    if (c.dtype == WD_DTYPE_BF16)
+      WD_TRY(gemm<uint16_t>(s, (const uint16_t*)s->a_act, c.hidden, m.lm, m.slm, s->logits, n,
+                            c.vocab, c.hidden, 1, &S));
+    else
+      WD_TRY(gemm<float>(s, (const float*)s->a_act, c.hidden, m.lm, nullptr, s->logits, n,
+                         c.vocab, c.hidden, 1, &S));
+    WD_HIP(wd::confidence(s->logits, n, c.vocab, c.mask_id, s->act_tok, s->act_conf,
+                          s->conf_scratch, m.stream));
+    s->logits_valid = true;
+  }
   const WdStepGeom g = base_geom(s);
   WD_HIP(wd::select_update(s->act_pos, s->act_tok, s->act_conf, n_act, s->win.unmask_per_step, g,
                            s->seq_len, s->x, s->dec, s->sel_pos, s->sel_tok, s->sel_conf, m.stream));
@@ -1395,9 +1423,17 @@ wd_status wd_seq_ends(const wd_seq* s, int32_t* ends) {
   return WD_OK;
 }
 
+wd_status wd_debug_keep_logits(wd_seq* s, int32_t on) {
+  if (!s) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  s->keep_logits = on != 0;
+  return WD_OK;
+}
+
 wd_status wd_debug_logits(const wd_seq* s, float* logits, int32_t* positions, int32_t capacity,
                           int32_t* n_rows) {
   if (!s || !logits || !n_rows) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  if (!s->logits_valid)
+    return fail(WD_ERR_STATE, "no logits kept for the last step (wd_debug_keep_logits)");
   const int n = s->B * s->last_nA;
   *n_rows = n;
   if (capacity < n) return fail(WD_ERR_OUT_OF_MEMORY, "capacity %d < %d rows", capacity, n);

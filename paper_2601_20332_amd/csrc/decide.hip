@@ -99,6 +99,53 @@ hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* t
   return hipGetLastError();
 }
 
+// Merge of the LM head's per-tile (max, argmax, sum exp) of one row: each
+// thread takes tiles tid, tid + 256, ... in order, then a fixed tree over the
+// block; the same rules (lowest id on ties, sums rescaled to the row max).
+__global__ __launch_bounds__(256) void k_conf_tiles(const float* __restrict__ pmax,
+                                                    const int* __restrict__ pidx,
+                                                    const float* __restrict__ psum, int n_tiles,
+                                                    int32_t* __restrict__ tok,
+                                                    float* __restrict__ conf) {
+  __shared__ float bv[4], ss[4];
+  __shared__ int bi[4];
+  const long base = (long)blockIdx.x * n_tiles;
+  float best = -INFINITY;
+  int idx = INT_MAX;
+  for (int t = threadIdx.x; t < n_tiles; t += blockDim.x) better(best, idx, pmax[base + t], pidx[base + t]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) better(best, idx, __shfl_xor(best, o, 64), __shfl_xor(idx, o, 64));
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    bv[w] = best;
+    bi[w] = idx;
+  }
+  __syncthreads();
+  best = bv[0];
+  idx = bi[0];
+  for (int i = 1; i < 4; ++i) better(best, idx, bv[i], bi[i]);
+  float s = 0.f;
+  if (best > -INFINITY)
+    for (int t = threadIdx.x; t < n_tiles; t += blockDim.x) {
+      const float m = pmax[base + t];
+      if (m > -INFINITY) s += psum[base + t] * expf(m - best);
+    }
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) ss[w] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    tok[blockIdx.x] = idx;
+    conf[blockIdx.x] = 1.0f / (ss[0] + ss[1] + ss[2] + ss[3]);
+  }
+}
+
+hipError_t confidence_tiles(const float* pmax, const int* pidx, const float* psum, int n,
+                            int n_tiles, int32_t* tok, float* conf, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_conf_tiles, dim3(n), dim3(256), 0, st, pmax, pidx, psum, n_tiles, tok, conf);
+  return hipGetLastError();
+}
+
 // ---- block-wide exclusive prefix count of a flag (blockDim.x multiple of 64) ----------
 __device__ __forceinline__ int block_prefix(bool f, int* wtot, int& total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;

@@ -12,6 +12,8 @@
 // launch has enough workgroups to keep every CU's memory pipeline full.
 #include <hip/hip_ext.h>
 
+#include <climits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -346,6 +348,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 // heads (RoPE pairs meet in lanes l and l ^ 32), rounds to T, stores q rows and
 // scatters k/v rows into the cache at row_tok.
 // EPI == kEpiSwiGlu: weights packed kPackGateUp.  out[m][f] = silu(g) * u.
+// EPI == kEpiConf (LM head): reduces the tile's 64 vocabulary entries of each
+// row to (max logit, lowest id reaching it, sum exp(l - max)), [MASK]
+// excluded, into pmax / pidx / psum[m][tile]; writes the logits themselves
+// only when ep.logits is set.
 struct FusedEpi {
   // Q/K/V
   const uint16_t* bias;     // [(nh + 2 nkv) * 128] or null
@@ -358,6 +364,11 @@ struct FusedEpi {
   // SwiGLU
   uint16_t* out;
   int F;
+  // LM head + confidence
+  int mask_id, n_tiles;
+  float* logits;            // [M][V] fp32, or null
+  float *pmax, *psum;       // [M][n_tiles]
+  int* pidx;
 };
 
 template <int EPI, int MF, int U, bool W8>
@@ -501,6 +512,70 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restr
       w.y = (uint32_t)f2bf(x[2]) | ((uint32_t)f2bf(x[3]) << 16);
       *(u32x2*)(dst + dim0) = w;
     }
+  } else if constexpr (EPI == kEpiConf) {
+    // lane: vocabulary ids v0 .. v0 + 3 of rows jf * 16 + lane % 16
+    __shared__ float cm[kWaves][16 * MF], cs[kWaves][16 * MF];
+    __shared__ int ci[kWaves][16 * MF];
+    const int v0 = grp * 16 + (lane >> 4) * 4;
+    const int N4 = N;
+#pragma unroll
+    for (int jf = 0; jf < MF; ++jf) {
+      const int m = jf * 16 + (lane & 15);
+      if (ep.logits && m < M) *(f32x4*)(ep.logits + (long)m * N4 + v0) = acc[jf];
+      float bm = -INFINITY;
+      int bi = INT_MAX;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (v0 + j != ep.mask_id && acc[jf][j] > bm) {
+          bm = acc[jf][j];
+          bi = v0 + j;
+        }
+#pragma unroll
+      for (int o = 16; o < 64; o <<= 1) {
+        const float om = __shfl_xor(bm, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (om > bm || (om == bm && oi < bi)) {
+          bm = om;
+          bi = oi;
+        }
+      }
+      if (lane < 16) {
+        cm[wave][jf * 16 + lane] = bm;
+        ci[wave][jf * 16 + lane] = bi;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int jf = 0; jf < MF; ++jf) {
+      const int r = jf * 16 + (lane & 15);
+      float mx = cm[0][r];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) mx = fmaxf(mx, cm[w][r]);
+      float sum = 0.f;
+      if (mx > -INFINITY)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (v0 + j != ep.mask_id) sum += expf(acc[jf][j] - mx);
+      sum += __shfl_xor(sum, 16, 64);
+      sum += __shfl_xor(sum, 32, 64);
+      if (lane < 16) cs[wave][r] = sum;
+    }
+    __syncthreads();
+    if (tid < 16 * MF && tid < M) {
+      const int r = tid;
+      float bm = cm[0][r];
+      int bi = ci[0][r];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w)
+        if (cm[w][r] > bm || (cm[w][r] == bm && ci[w][r] < bi)) {
+          bm = cm[w][r];
+          bi = ci[w][r];
+        }
+      const long o = (long)r * ep.n_tiles + nb;
+      ep.pmax[o] = bm;
+      ep.pidx[o] = bi;
+      ep.psum[o] = cs[0][r] + cs[1][r] + cs[2][r] + cs[3][r];
+    }
   } else {
     const int f0 = grp * 8 + sub;         // this lane's features f0 .. f0 + 3
 #pragma unroll
@@ -572,6 +647,19 @@ hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M
   ep.vc = vc;
   ep.cache_rows = cache_rows;
   return launch_fused<kEpiQkv, 8>(X, ldx, Wp, M, N, K, ep, wsc, st, e0, e1);
+}
+
+hipError_t gemm_bf16_lmhead_conf(const uint16_t* X, int ldx, const void* Wp, int M, int V, int K,
+                                 int mask_id, float* logits, float* pmax, int* pidx, float* psum,
+                                 hipStream_t st, hipEvent_t e0, hipEvent_t e1, const float* wsc) {
+  FusedEpi ep{};
+  ep.mask_id = mask_id;
+  ep.n_tiles = V / 64;
+  ep.logits = logits;
+  ep.pmax = pmax;
+  ep.pidx = pidx;
+  ep.psum = psum;
+  return launch_fused<kEpiConf, 8>(X, ldx, Wp, M, V, K, ep, wsc, st, e0, e1);
 }
 
 hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, int M, int F, int K,

@@ -35,7 +35,7 @@ hipError_t pack_fp8(const uint16_t* W, int N, int K, void* out, float* scale, hi
 // kPackRopePair, head_dim 128; writes q [M][nh][128] and the k/v cache rows
 // row_tok of each head.  SwiGLU: weights packed kPackGateUp (N = 2F);
 // writes out [M][F] = silu(gate) * up.
-constexpr int kEpiQkv = 1, kEpiSwiGlu = 2;
+constexpr int kEpiQkv = 1, kEpiSwiGlu = 2, kEpiConf = 3;
 bool fused_rows_ok(int M, int N, int K);
 hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
                                const uint16_t* bias, const float* rope_cs, const int32_t* row_pos,
@@ -43,6 +43,14 @@ hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M
                                uint16_t* vc, long cache_rows, hipStream_t st,
                                hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr,
                                const float* wsc = nullptr);
+// LM head with the confidence reduction in the kernel: per row and 64-entry
+// vocabulary tile, (max logit, lowest id reaching it, sum exp(l - max)),
+// [MASK] excluded, at [row][tile] of pmax / pidx / psum (V / 64 tiles);
+// logits [M][V] are written only if non-null.  confidence_tiles merges them.
+hipError_t gemm_bf16_lmhead_conf(const uint16_t* X, int ldx, const void* Wp, int M, int V, int K,
+                                 int mask_id, float* logits, float* pmax, int* pidx, float* psum,
+                                 hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr,
+                                 const float* wsc = nullptr);
 hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, int M, int F, int K,
                                   uint16_t* out, hipStream_t st, hipEvent_t e0 = nullptr,
                                   hipEvent_t e1 = nullptr, const float* wsc = nullptr);
@@ -88,6 +96,9 @@ hipError_t attention_f32(const float* q, const float* kcache, const float* vcach
 // Two passes: kConfChunks vocabulary chunks per row into `scratch`
 // (3 * n * kConfChunks floats), then a per-row combine.
 constexpr int kConfChunks = 16;
+// Merges the per-tile reductions of gemm_bf16_lmhead_conf in tile order.
+hipError_t confidence_tiles(const float* pmax, const int* pidx, const float* psum, int n,
+                            int n_tiles, int32_t* tok, float* conf, hipStream_t st);
 hipError_t confidence(const float* logits, int n, int V, int mask_id, int32_t* tok, float* conf,
                       float* scratch, hipStream_t st);
 // Row set of a step, per sequence by g.mode[b]: 0 = refresh ([0, c)),

@@ -79,6 +79,7 @@ def run_gpu(model, prompts, gen_len, win: synth.WindowSettings, full: bool = Fal
     gen = wd.wd_prefill_prompt(model, prompts, gen_len, wc)
     steps = []
     try:
+        wd.wd_debug_keep_logits(gen, keep_logits)
         n = 0
         while max_steps is None or n < max_steps:
             try:
