@@ -13,6 +13,7 @@
 #include <hip/hip_ext.h>
 
 #include <climits>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -201,12 +202,18 @@ constexpr int kWaves = 4;
 // With a start/stop event pair, the launch records them from its own dispatch
 // (the kernel's execution time, as a kernel trace reports it).
 template <typename F, typename... A>
+static void launch_timed_block(F kernel, dim3 grid, dim3 block, hipStream_t st, hipEvent_t e0,
+                               hipEvent_t e1, A... args) {
+  if (e0)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, e0, e1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+}
+
+template <typename F, typename... A>
 static void launch_timed(F kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
                          A... args) {
-  if (e0)
-    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, args...);
-  else
-    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, args...);
+  launch_timed_block(kernel, grid, dim3(256), st, e0, e1, args...);
 }
 
 
@@ -334,13 +341,15 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 
 
 // ---- few-row GEMM with its epilogue, no K split ----------------------------------------
-// For the wide products of a normal step (Q/K/V, gate/up) the whole K range of
-// a 64-feature tile is one workgroup, so its sums are final and the epilogue
-// runs in the kernel: no split-K partials and no epilogue launch.  Same tile
-// as k_gemm_bf16 (4 waves, one 16-row weight group each, activations staged
-// through LDS); the weights of iteration it + 2 are in flight while
-// iteration it is computed (a ring of three register buffers), the
-// activations of it + 1 go to the other half of a double-buffered LDS tile.
+// For the wide products of a normal step (Q/K/V, gate/up, LM head) the whole
+// K range of a tile of GW 16-feature weight groups is one workgroup (one wave
+// per group), so its sums are final and the epilogue runs in the kernel: no
+// split-K partials and no epilogue launch.  Activations are staged through
+// LDS and shared by the waves.  Every iteration waits on loads issued several
+// iterations earlier: the weights of iteration it + 3 are loaded while it is
+// computed (a ring of four register buffers), the activations of it + 2 go to
+// registers and those of it + 1 to the other half of a double-buffered LDS
+// tile, so neither stream pays a full memory round trip per iteration.
 // Loads read clamped addresses, so they are never predicated; K steps past
 // the end are zeroed when stored to LDS and their products add nothing.
 //
@@ -371,23 +380,30 @@ struct FusedEpi {
   int* pidx;
 };
 
-template <int EPI, int MF, int U, bool W8>
-__global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restrict__ X, int ldx,
-                                                         const u32x4* __restrict__ Wp, int M, int N,
-                                                         int K, FusedEpi ep,
-                                                         const float* __restrict__ wsc) {
+template <int V>
+using ic = std::integral_constant<int, V>;
+
+template <int EPI, int MF, int U, bool W8, int GW>
+__global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __restrict__ X, int ldx,
+                                                             const u32x4* __restrict__ Wp, int M,
+                                                             int N, int K, FusedEpi ep,
+                                                             const float* __restrict__ wsc) {
+  static_assert(EPI != kEpiConf || GW == kWaves, "the confidence epilogue reduces 64-entry tiles");
+  constexpr int NT = 64 * GW;
+  constexpr int R = 4;   // weight ring: loads run R - 1 iterations ahead
+  constexpr int XD = 2;  // activations: loaded XD iterations ahead, staged one ahead
   constexpr int ROWS = 16 * MF;
   constexpr int PITCH = U * 32 + 8;
   constexpr int CHUNK16 = ROWS * U * 4;
-  constexpr int PER_T = (CHUNK16 + 255) / 256;
+  constexpr int PER_T = (CHUNK16 + NT - 1) / NT;
   __shared__ __attribute__((aligned(16))) uint16_t xs[2][ROWS * PITCH];
-  const int G = N / (16 * kWaves);
+  const int G = gridDim.x;
   int id = blockIdx.x;
   if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);
   const int nb = id;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int KT = K >> 5;
-  const int grp = nb * kWaves + wave;  // this wave's 16-row weight group
+  const int grp = nb * GW + wave;  // this wave's 16-row weight group
   // W8: the ring holds raw fp8 fragments (one per two K steps), decoded when used
   constexpr int UW = W8 ? U / 2 : U;
   const int frags = W8 ? KT / 2 : KT;
@@ -397,44 +413,48 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restr
   for (int b = 0; b < MF; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
   const u32x4 zero = {0u, 0u, 0u, 0u};
   const int n_it = (KT + U - 1) / U;
-  u32x4 pre[PER_T];
-  u32x4 a0[UW], a1[UW], a2[UW];
-  auto wload = [&](u32x4 (&a)[UW], int it) {
+  u32x4 pre[XD][PER_T];
+  u32x4 a[R][UW];
+  auto wload = [&](auto B, int it) {
+    constexpr int b = decltype(B)::value;
 #pragma unroll
     for (int u = 0; u < UW; ++u)
-      a[u] = __builtin_nontemporal_load(wp + (long)min(it * UW + u, frags - 1) * 64);
+      a[b][u] = __builtin_nontemporal_load(wp + (long)min(it * UW + u, frags - 1) * 64);
   };
-  auto xload = [&](int it) {
+  auto xload = [&](auto P, int it) {
+    constexpr int p = decltype(P)::value;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
-      const int e = min(tid + i * 256, CHUNK16 - 1);
+      const int e = min(tid + i * NT, CHUNK16 - 1);
       const int r = e / (U * 4), cc = e % (U * 4);
       const long row = min(r, M - 1);
       const int kc = min(it * U + cc / 4, KT - 1);
-      pre[i] = *(const u32x4*)(X + row * ldx + kc * 32 + (cc & 3) * 8);
+      pre[p][i] = *(const u32x4*)(X + row * ldx + kc * 32 + (cc & 3) * 8);
     }
   };
-  auto xstore = [&](int buf, int it) {
+  auto xstore = [&](auto P, int buf, int it) {
+    constexpr int p = decltype(P)::value;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
-      const int e = tid + i * 256;
-      if (CHUNK16 % 256 == 0 || e < CHUNK16) {
+      const int e = tid + i * NT;
+      if (CHUNK16 % NT == 0 || e < CHUNK16) {
         const int r = e / (U * 4), cc = e % (U * 4);
         const bool ok = r < M && it * U + cc / 4 < KT;
-        *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[i] : zero;
+        *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[p][i] : zero;
       }
     }
   };
-  auto compute = [&](const u32x4 (&a)[UW], int buf) {
+  auto compute = [&](auto B, int buf) {
+    constexpr int bsel = decltype(B)::value;
     const uint16_t* xb = xs[buf];
     constexpr int PAIR = W8 ? 2 : 1;  // K steps per weight register of the ring
 #pragma unroll
     for (int uw = 0; uw < UW; ++uw) {
       u32x4 w[PAIR];
       if constexpr (W8)
-        fp8_frag_to_bf16(a[uw], w[0], w[1]);
+        fp8_frag_to_bf16(a[bsel][uw], w[0], w[1]);
       else
-        w[0] = a[uw];
+        w[0] = a[bsel][uw];
 #pragma unroll
       for (int h = 0; h < PAIR; ++h) {
         const int u = uw * PAIR + h;
@@ -447,22 +467,27 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_fused(const uint16_t* __restr
       }
     }
   };
-  auto body = [&](u32x4 (&cur)[UW], u32x4 (&ld)[UW], int it) {
-    xload(it + 1);
-    wload(ld, it + 2);
-    if (it < n_it) compute(cur, it & 1);
-    xstore((it + 1) & 1, it + 1);
+  // iteration it = base + J with base a multiple of R (and of XD): buffers are static
+  auto body = [&](auto J, int it) {
+    constexpr int j = decltype(J)::value;
+    xload(ic<j % XD>{}, it + XD);
+    wload(ic<(j + R - 1) % R>{}, it + R - 1);
+    if (it < n_it) compute(ic<j % R>{}, j & 1);
+    xstore(ic<(j + 1) % XD>{}, (j + 1) & 1, it + 1);
     __syncthreads();
   };
-  xload(0);
-  wload(a0, 0);
-  wload(a1, 1);
-  xstore(0, 0);
+  xload(ic<0>{}, 0);
+  xload(ic<1>{}, 1);
+  wload(ic<0>{}, 0);
+  wload(ic<1>{}, 1);
+  wload(ic<2>{}, 2);
+  xstore(ic<0>{}, 0, 0);
   __syncthreads();
-  for (int it = 0; it < n_it; it += 3) {
-    body(a0, a2, it);
-    body(a1, a0, it + 1);
-    body(a2, a1, it + 2);
+  for (int it = 0; it < n_it; it += R) {
+    body(ic<0>{}, it);
+    body(ic<1>{}, it + 1);
+    body(ic<2>{}, it + 2);
+    body(ic<3>{}, it + 3);
   }
 
   // lane l holds packed rows grp*16 + (l/16)*4 + j (j < 4) of activation rows
@@ -603,29 +628,47 @@ bool fused_rows_ok(int M, int N, int K) {
   return M >= 1 && M <= 64 && N % 64 == 0 && K % 32 == 0 && N / 64 >= 192;
 }
 
-template <int EPI, int U, bool W8>
+template <int EPI, int U, bool W8, int GW>
 static void launch_fused_mf(dim3 grid, int M, const uint16_t* X, int ldx, const u32x4* W, int N,
                             int K, const FusedEpi& ep, const float* wsc, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1) {
+  const dim3 block(64 * GW);
   switch ((M + 15) / 16) {
-    case 1: launch_timed(k_gemm_bf16_fused<EPI, 1, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
-    case 2: launch_timed(k_gemm_bf16_fused<EPI, 2, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
-    case 3: launch_timed(k_gemm_bf16_fused<EPI, 3, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
-    default: launch_timed(k_gemm_bf16_fused<EPI, 4, U, W8>, grid, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 1: launch_timed_block(k_gemm_bf16_fused<EPI, 1, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 2: launch_timed_block(k_gemm_bf16_fused<EPI, 2, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 3: launch_timed_block(k_gemm_bf16_fused<EPI, 3, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    default: launch_timed_block(k_gemm_bf16_fused<EPI, 4, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
   }
 }
 
+// GW weight groups (16 features each) per workgroup, one wave each: 4 by
+// default; 6 when that gives at least one workgroup per CU, which spreads a
+// wide matrix (gate/up) evenly over the 256 CUs instead of 1.5 workgroups per CU.
 template <int EPI, int U>
 static hipError_t launch_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
                                const FusedEpi& ep, const float* wsc, hipStream_t st, hipEvent_t e0,
                                hipEvent_t e1) {
   if (!fused_rows_ok(M, N, K) || (wsc && K % 64)) return hipErrorInvalidValue;
-  const dim3 grid(N / 64);
   const u32x4* W = (const u32x4*)Wp;
-  if (wsc)
-    launch_fused_mf<EPI, U, true>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
-  else
-    launch_fused_mf<EPI, U, false>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
+  const int groups = N / 16;
+  bool six = false;
+  if constexpr (EPI != kEpiConf) {
+    six = groups % 6 == 0 && groups / 6 >= 256;
+    if (six) {
+      const dim3 grid(groups / 6);
+      if (wsc)
+        launch_fused_mf<EPI, U, true, 6>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
+      else
+        launch_fused_mf<EPI, U, false, 6>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
+    }
+  }
+  if (!six) {
+    const dim3 grid(groups / 4);
+    if (wsc)
+      launch_fused_mf<EPI, U, true, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
+    else
+      launch_fused_mf<EPI, U, false, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
+  }
   return hipGetLastError();
 }
 
@@ -646,7 +689,7 @@ hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M
   ep.kc = kc;
   ep.vc = vc;
   ep.cache_rows = cache_rows;
-  return launch_fused<kEpiQkv, 8>(X, ldx, Wp, M, N, K, ep, wsc, st, e0, e1);
+  return launch_fused<kEpiQkv, 4>(X, ldx, Wp, M, N, K, ep, wsc, st, e0, e1);
 }
 
 hipError_t gemm_bf16_lmhead_conf(const uint16_t* X, int ldx, const void* Wp, int M, int V, int K,
@@ -659,7 +702,7 @@ hipError_t gemm_bf16_lmhead_conf(const uint16_t* X, int ldx, const void* Wp, int
   ep.pmax = pmax;
   ep.pidx = pidx;
   ep.psum = psum;
-  return launch_fused<kEpiConf, 8>(X, ldx, Wp, M, V, K, ep, wsc, st, e0, e1);
+  return launch_fused<kEpiConf, 4>(X, ldx, Wp, M, V, K, ep, wsc, st, e0, e1);
 }
 
 hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, int M, int F, int K,
