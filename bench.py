@@ -231,6 +231,63 @@ def fp8_weight_variant(model8, prompts, w, n_steps, fixed_s):
     }
 
 
+def other_workload(name: str, device: str):
+    """Windowed generation on a second workload shape (one model upload, one
+    warm-up, two timed generations, one full-sequence generation for the
+    speedup, one instrumented generation for the GEMM rooflines)."""
+    import paper_2601_20332_amd as wd
+    import synth
+    import torch
+    w = synth.WORKLOADS[name]
+    t0 = time.time()
+    model = upload_model(w.model, device)
+    log(f"[bench] {name}: weights generated and packed in {time.time() - t0:.1f}s")
+    prompts = synth.prompts(w.model, synth.prompt_lengths(w))
+    win = w.window
+    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
+    n_steps = len(wd.wd_plan(w.prompt_len, w.gen_len, wc)["n_rows"])
+    generation(model, prompts, w.gen_len, wc, n_steps)
+    torch.cuda.synchronize()
+    reps = 2
+    t1 = time.perf_counter()
+    for _ in range(reps):
+        generation(model, prompts, w.gen_len, wc, n_steps)
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t1) / reps
+    tf = time.perf_counter()
+    generation(model, prompts, w.gen_len, wc, n_steps, full=True)
+    torch.cuda.synchronize()
+    t_full = time.perf_counter() - tf
+    wd.wd_profile_enable(model, True)
+    te = time.perf_counter()
+    generation(model, prompts, w.gen_len, wc, n_steps)
+    torch.cuda.synchronize()
+    te = time.perf_counter() - te
+    rows = roofline_of(model, wd.WD_PROF_GEMM_ROWS, te)
+    tiled = roofline_of(model, wd.WD_PROF_GEMM_TILED, te)
+    wd.wd_profile_enable(model, False)
+    model.free()
+    for r in (rows, tiled):
+        if r:
+            r["traffic"] = None  # the counter runs cover the LLaDA-8B workload
+    B = len(prompts)
+    m = w.model
+    return {
+        "workload": (f"{name}: {m.n_layers}L hidden {m.hidden} {m.n_heads}q/{m.n_kv_heads}kv x "
+                     f"{m.head_dim} ffn {m.ffn} vocab {m.vocab}{' qkv bias' if m.qkv_bias else ''}, "
+                     f"random init N(0,0.02)"),
+        "batch": B, "prompt_len": w.prompt_len, "gen_len": w.gen_len,
+        "n_active": win.n_active, "n_buffer": win.n_buffer, "refresh_every": win.refresh_every,
+        "unmask_per_step": win.unmask_per_step,
+        "steps_per_s": round(n_steps / t, 3),
+        "decoded_tokens_per_s": round(B * w.gen_len / t, 3),
+        "ms_per_generation": round(t * 1e3, 2),
+        "speedup_vs_full_sequence": round(t_full / t, 3),
+        "roofline": rows,
+        "roofline_tiled_gemm": tiled,
+    }
+
+
 def generation(model, prompts, G, wc, n_steps, full=False):
     import paper_2601_20332_amd as wd
     gen = wd.wd_prefill_prompt(model, prompts, G, wc)
@@ -406,6 +463,8 @@ def main():
                     help="skip the adaptive-termination measurement")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the buffer-only refresh variant")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the second workload shape (Dream-7B) and the peak probe")
     ap.add_argument("--no-events", action="store_true",
                     help="time without the per-launch GEMM events (no roofline)")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
@@ -508,7 +567,27 @@ def main():
     if not args.no_eos:
         adaptive = adaptive_termination(model, prompts, w, n_steps, elapsed / args.steps)
         log(f"[bench] adaptive termination: {adaptive}")
+    peaks = None
+    if not args.no_others:
+        tf_meas, gbs_meas = wd.wd_measure_peaks(model)
+        peaks = {"mfma_bf16_tflops": round(tf_meas, 1), "hbm_read_gbs": round(gbs_meas, 1),
+                 "method": "independent 32x32x16 bf16 MFMAs on every CU; one non-temporal "
+                           "read pass over 4 GiB"}
+        log(f"[bench] measured peaks: {peaks}")
+        for r in (roofline, roofline_tiled):
+            if r:
+                meas = gbs_meas if r["unit"] == "GB/s" else tf_meas
+                r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
     model.free()
+    others = None
+    if not args.no_others and args.workload == "llada8b":
+        others = {"dream7b": other_workload("dream7b", device)}
+        log(f"[bench] dream7b: {others['dream7b']}")
+        if peaks:
+            for r in (others["dream7b"]["roofline"], others["dream7b"]["roofline_tiled_gemm"]):
+                if r:
+                    meas = peaks["hbm_read_gbs"] if r["unit"] == "GB/s" else peaks["mfma_bf16_tflops"]
+                    r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -552,6 +631,8 @@ def main():
         "adaptive_termination": adaptive,
         "buffer_refresh_variant": variant,
         "fp8_weight_variant": fp8,
+        "measured_peaks": peaks,
+        "other_workloads": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -293,7 +293,9 @@ enum {
  * gate/up, down and LM-head products) on this model's stream records a pair
  * of HIP events from its own dispatch (start and end of the kernel), and the
  * launch's kernel class and algorithmic traffic and work are recorded: bytes = weights (N*K elements) + input rows (M*K
- * elements) + fp32 output (M*N*4), flops = 2*M*N*K.  Up to 1 << 20 launches
+ * elements) + what the launch writes (fp32 M*N*4 for a split-K launch, the
+ * bf16 results of a fused Q/K/V or SwiGLU launch, 12 bytes per row and
+ * 64-entry vocabulary tile for the fused LM head), flops = 2*M*N*K.  Up to 1 << 20 launches
  * are kept (WD_ERR_OUT_OF_MEMORY from the launching call beyond that).
  * Disabled by default; every call discards the records taken so far. */
 wd_status wd_profile_enable(wd_model* m, int32_t enable);
@@ -306,6 +308,14 @@ wd_status wd_profile_enable(wd_model* m, int32_t enable);
  * WD_ERR_INVALID_ARG. */
 wd_status wd_profile_read(wd_model* m, int32_t kernel, int64_t* launches, double* total_ms,
                           double* alg_bytes, double* alg_flops);
+
+/* Measures, on the model's device and stream, the achievable dense bf16
+ * matrix-core throughput (a loop of independent 32x32x16 MFMAs on every CU,
+ * TFLOP/s) and HBM read bandwidth (one non-temporal pass over a 4 GiB
+ * buffer, GB/s); the better of two timed runs each.  Allocates and frees the
+ * 4 GiB buffer itself; synchronizes.  For reporting roofline fractions
+ * against measured as well as vendor peaks. */
+wd_status wd_measure_peaks(wd_model* m, double* mfma_bf16_tflops, double* hbm_read_gbs);
 
 /* ---- host-only helpers -------------------------------------------------------- */
 

@@ -30,7 +30,7 @@ EXPORTED = ["wd_weight_count", "wd_weight_shape", "wd_model_bytes", "wd_init_mod
             "wd_free_model", "wd_seq_bytes", "wd_prefill_prompt", "wd_slide_window",
             "wd_refresh_buffer", "wd_step", "wd_full_step", "wd_get_state", "wd_debug_logits",
             "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error", "wd_profile_enable",
-            "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row", "wd_debug_keep_logits"]
+            "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row", "wd_debug_keep_logits", "wd_measure_peaks"]
 
 
 class WdError(RuntimeError):
@@ -106,6 +106,7 @@ def _load() -> ctypes.CDLL:
         "wd_plan": (i32, [i32, i32, ctypes.POINTER(WindowConfig), i32, pi32, pi32, pi32, pi32, pi32]),
         "wd_last_error": (ctypes.c_char_p, []),
         "wd_profile_enable": (i32, [P, i32]),
+        "wd_measure_peaks": (i32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
         "wd_profile_read": (i32, [P, i32, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     }
@@ -373,6 +374,13 @@ def wd_profile_read(model: Model, kernel: int = WD_PROF_ALL):
     _check(lib.wd_profile_read(model.handle, int(kernel), ctypes.byref(n), ctypes.byref(ms),
                                ctypes.byref(by), ctypes.byref(fl)))
     return n.value, ms.value, by.value, fl.value
+
+
+def wd_measure_peaks(model: Model):
+    """(dense bf16 MFMA TFLOP/s, HBM read GB/s) measured on the model's GPU."""
+    t, g = ctypes.c_double(), ctypes.c_double()
+    _check(lib.wd_measure_peaks(model.handle, ctypes.byref(t), ctypes.byref(g)))
+    return t.value, g.value
 
 
 def wd_last_error() -> str:

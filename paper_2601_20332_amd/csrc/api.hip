@@ -582,6 +582,14 @@ wd_status wd_profile_enable(wd_model* m, int32_t enable) {
   return WD_OK;
 }
 
+wd_status wd_measure_peaks(wd_model* m, double* mfma_bf16_tflops, double* hbm_read_gbs) {
+  if (!m || !mfma_bf16_tflops || !hbm_read_gbs) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  if (hipSetDevice(m->device) != hipSuccess) return fail(WD_ERR_DEVICE, "hipSetDevice failed");
+  WD_HIP(hipStreamSynchronize(m->stream));
+  WD_HIP(wd::measure_peaks(m->stream, mfma_bf16_tflops, hbm_read_gbs));
+  return WD_OK;
+}
+
 wd_status wd_profile_read(wd_model* m, int32_t kernel, int64_t* launches, double* total_ms,
                           double* alg_bytes, double* alg_flops) {
   if (!m) return fail(WD_ERR_INVALID_ARG, "model is NULL");

@@ -96,6 +96,10 @@ hipError_t attention_f32(const float* q, const float* kcache, const float* vcach
 // Two passes: kConfChunks vocabulary chunks per row into `scratch`
 // (3 * n * kConfChunks floats), then a per-row combine.
 constexpr int kConfChunks = 16;
+// Achievable dense bf16 MFMA TFLOP/s and HBM read GB/s (4 GiB allocated and
+// freed here); synchronizes the stream.
+hipError_t measure_peaks(hipStream_t st, double* mfma_tflops, double* read_gbs);
+
 // Merges the per-tile reductions of gemm_bf16_lmhead_conf in tile order.
 hipError_t confidence_tiles(const float* pmax, const int* pidx, const float* psum, int n,
                             int n_tiles, int32_t* tok, float* conf, hipStream_t st);

@@ -215,3 +215,17 @@ def test_profile_records_by_kernel_class():
         wd.wd_profile_read(m, 7)
     wd.wd_profile_enable(m, False)
     m.free()
+
+
+def test_measured_peaks_are_plausible():
+    """The peak probe's two kernels run and report numbers of the right order
+    for an MI355X (vendor peaks: 2.5 PFLOP/s dense bf16, 8 TB/s)."""
+    W = synth.Weights(MICRO_MHA)
+    m = gpu_model(W)
+    try:
+        tflops, gbs = wd.wd_measure_peaks(m)
+    finally:
+        m.free()
+    print(f"PEAKS mfma_bf16={tflops:.1f} TFLOP/s hbm_read={gbs:.1f} GB/s", flush=True)
+    assert 200.0 < tflops < 2600.0
+    assert 1000.0 < gbs < 8200.0
