@@ -49,6 +49,7 @@ def gemm_source_hash() -> str:
 
 # GEMM kernel classes of wd_profile_read and the kernel each one is
 KERNEL_CLASSES = {1: "k_gemm_bf16", 2: "k_gemm_bf16_big"}
+PROFILE_NAMES = {**KERNEL_CLASSES, 4: "k_attn_bf16"}
 
 
 def measured_traffic(kernel: str):
@@ -147,14 +148,16 @@ def roofline_of(model, kernel_class: int, elapsed_ev: float):
     launches, ms, alg_bytes, alg_flops = wd.wd_profile_read(model, kernel_class)
     if launches <= 0 or ms <= 0:
         return None
-    name = KERNEL_CLASSES[kernel_class]
+    name = PROFILE_NAMES[kernel_class]
     avg_s = ms / 1e3 / launches
     gbs = alg_bytes / launches / avg_s / 1e9
     tfs = alg_flops / launches / avg_s / 1e12
-    hbm = kernel_class == 1
+    hbm = kernel_class in (1, 4)
     achieved, peak = (gbs, HBM_PEAK_GBS) if hbm else (tfs, BF16_PEAK_TFLOPS)
+    label = {1: " + k_gemm_bf16_fused (at most 64 rows)", 2: " (128-row tiles)",
+             4: " + k_attn_combine (one layer's attention)"}[kernel_class]
     return {
-        "kernel": name + (" + k_gemm_bf16_fused (at most 64 rows)" if hbm else " (128-row tiles)"),
+        "kernel": name + label,
         "bound": "hbm" if hbm else "mfma",
         "achieved": round(achieved, 1),
         "peak": peak,
@@ -265,9 +268,10 @@ def other_workload(name: str, device: str):
     te = time.perf_counter() - te
     rows = roofline_of(model, wd.WD_PROF_GEMM_ROWS, te)
     tiled = roofline_of(model, wd.WD_PROF_GEMM_TILED, te)
+    attn = roofline_of(model, wd.WD_PROF_ATTN, te)
     wd.wd_profile_enable(model, False)
     model.free()
-    for r in (rows, tiled):
+    for r in (rows, tiled, attn):
         if r:
             r["traffic"] = None  # the counter runs cover the LLaDA-8B workload
     B = len(prompts)
@@ -285,6 +289,7 @@ def other_workload(name: str, device: str):
         "speedup_vs_full_sequence": round(t_full / t, 3),
         "roofline": rows,
         "roofline_tiled_gemm": tiled,
+        "roofline_attention": attn,
     }
 
 
@@ -528,7 +533,7 @@ def main():
     # Roofline of the dominant kernel: the same generations again, now with a
     # HIP event pair around every projection-GEMM launch on the library's stream
     # (kept out of the pass above, whose clock gives `value`).
-    roofline = roofline_tiled = None
+    roofline = roofline_tiled = roofline_attn = None
     if not args.no_events:
         wd.wd_profile_enable(model, True)
         torch.cuda.synchronize()
@@ -541,6 +546,8 @@ def main():
         roofline = roofline_of(model, wd.WD_PROF_GEMM_ROWS, elapsed_ev)
         # second: the 128-row-tile GEMM of the refresh steps
         roofline_tiled = roofline_of(model, wd.WD_PROF_GEMM_TILED, elapsed_ev)
+        # attention: K/V of [0, c) streamed per layer and step
+        roofline_attn = roofline_of(model, wd.WD_PROF_ATTN, elapsed_ev)
         wd.wd_profile_enable(model, False)
         if roofline:
             roofline["instrumented_pass_s"] = round(elapsed_ev, 3)
@@ -574,7 +581,7 @@ def main():
                  "method": "independent 32x32x16 bf16 MFMAs on every CU; one non-temporal "
                            "read pass over 4 GiB"}
         log(f"[bench] measured peaks: {peaks}")
-        for r in (roofline, roofline_tiled):
+        for r in (roofline, roofline_tiled, roofline_attn):
             if r:
                 meas = gbs_meas if r["unit"] == "GB/s" else tf_meas
                 r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
@@ -584,7 +591,8 @@ def main():
         others = {"dream7b": other_workload("dream7b", device)}
         log(f"[bench] dream7b: {others['dream7b']}")
         if peaks:
-            for r in (others["dream7b"]["roofline"], others["dream7b"]["roofline_tiled_gemm"]):
+            for r in (others["dream7b"]["roofline"], others["dream7b"]["roofline_tiled_gemm"],
+                      others["dream7b"]["roofline_attention"]):
                 if r:
                     meas = peaks["hbm_read_gbs"] if r["unit"] == "GB/s" else peaks["mfma_bf16_tflops"]
                     r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
@@ -628,6 +636,7 @@ def main():
         "speedup_vs_full_sequence": full_speedup,
         "roofline": roofline,
         "roofline_tiled_gemm": roofline_tiled,
+        "roofline_attention": roofline_attn,
         "adaptive_termination": adaptive,
         "buffer_refresh_variant": variant,
         "fp8_weight_variant": fp8,

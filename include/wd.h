@@ -286,7 +286,11 @@ enum {
                              steps, LM head) */
   WD_PROF_GEMM_TILED = 2, /* k_gemm_bf16_big: more than 64 rows in 128-row tiles (refresh
                              and full-sequence steps) */
-  WD_PROF_GEMM_F32 = 3    /* k_gemm_f32: fp32 models */
+  WD_PROF_GEMM_F32 = 3,   /* k_gemm_f32: fp32 models */
+  WD_PROF_ATTN = 4        /* bf16 attention of one layer (k_attn_bf16 and, when the keys are
+                             split, k_attn_combine, timed as one unit); bytes = K and V rows
+                             [0, c) of every sequence + the q rows read + the output rows
+                             written, flops = 4 * rows * c * n_heads * head_dim */
 };
 
 /* When enabled, every launch of the projection GEMM kernels (Q/K/V, output,

@@ -364,7 +364,7 @@ def wd_profile_enable(model: Model, enable: bool = True) -> None:
 
 
 # kernel classes of wd_profile_read
-WD_PROF_ALL, WD_PROF_GEMM_ROWS, WD_PROF_GEMM_TILED, WD_PROF_GEMM_F32 = 0, 1, 2, 3
+WD_PROF_ALL, WD_PROF_GEMM_ROWS, WD_PROF_GEMM_TILED, WD_PROF_GEMM_F32, WD_PROF_ATTN = 0, 1, 2, 3, 4
 
 
 def wd_profile_read(model: Model, kernel: int = WD_PROF_ALL):

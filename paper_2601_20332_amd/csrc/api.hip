@@ -593,7 +593,7 @@ wd_status wd_measure_peaks(wd_model* m, double* mfma_bf16_tflops, double* hbm_re
 wd_status wd_profile_read(wd_model* m, int32_t kernel, int64_t* launches, double* total_ms,
                           double* alg_bytes, double* alg_flops) {
   if (!m) return fail(WD_ERR_INVALID_ARG, "model is NULL");
-  if (kernel < WD_PROF_ALL || kernel > WD_PROF_GEMM_F32)
+  if (kernel < WD_PROF_ALL || kernel > WD_PROF_ATTN)
     return fail(WD_ERR_INVALID_ARG, "unknown kernel class %d", kernel);
   WD_HIP(hipStreamSynchronize(m->stream));
   int64_t n = 0;
@@ -829,6 +829,25 @@ wd_status profile_end(wd_model& m, int kind, int M, int N, int K, size_t esz,
   return WD_OK;
 }
 
+// One attention unit: K and V of [0, c) per sequence, q rows in, output rows out.
+wd_status profile_attention(wd_model& m, const WdStepGeom& g) {
+  if (!m.profile) return WD_OK;
+  const wd_model_config& c = m.cfg;
+  double bytes = 0, flops = 0;
+  for (int b = 0; b < g.batch; ++b) {
+    if (g.nrows[b] <= 0) continue;
+    bytes += 2.0 * g.ctx[b] * c.n_kv_heads * c.head_dim * m.esz;
+    bytes += 2.0 * g.nrows[b] * c.n_heads * c.head_dim * m.esz;
+    flops += 4.0 * g.nrows[b] * g.ctx[b] * c.n_heads * c.head_dim;
+  }
+  if (bytes == 0) return WD_OK;  // no rows: nothing was launched, the events stay unused
+  m.rec_bytes.push_back(bytes);
+  m.rec_flops.push_back(flops);
+  m.rec_kind.push_back(WD_PROF_ATTN);
+  m.n_rec++;
+  return WD_OK;
+}
+
 template <typename T>
 wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, const float* wsc, float* C,
                       int M, int N, int K, int max_splits, int* splits, int* kind, hipEvent_t e0,
@@ -906,9 +925,12 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
                                  c.n_heads, c.n_kv_heads, c.head_dim, q, kc, vc, s->T, st));
     }
     if (c.dtype == WD_DTYPE_BF16) {
+      hipEvent_t e0, e1;
+      WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::attention_bf16((const uint16_t*)q, (const uint16_t*)kc, (const uint16_t*)vc, s->T,
                                 (uint16_t*)o, r.g, c.n_heads, c.n_kv_heads, c.head_dim,
-                                s->attn_part, s->attn_part_floats, st));
+                                s->attn_part, s->attn_part_floats, st, e0, e1));
+      WD_TRY(profile_attention(m_mut(s), r.g));
     } else {
       WD_HIP(wd::attention_f32((const float*)q, (const float*)kc, (const float*)vc, s->T,
                                (float*)o, s->row_seq, M, r.g, c.n_heads, c.n_kv_heads, c.head_dim,

@@ -87,7 +87,8 @@ hipError_t swiglu(const float* C, int S, int M, int F, T* out, hipStream_t st);
 // when it is too small.
 hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint16_t* vcache,
                           long cache_rows, uint16_t* o, const WdStepGeom& g, int n_heads, int n_kv,
-                          int head_dim, float* part, long part_floats, hipStream_t st);
+                          int head_dim, float* part, long part_floats, hipStream_t st,
+                          hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t attention_f32(const float* q, const float* kcache, const float* vcache, long cache_rows,
                          float* o, const int32_t* row_seq, int M, const WdStepGeom& g, int n_heads,
                          int n_kv, int head_dim, hipStream_t st);

@@ -5,6 +5,8 @@
 // are at index row_tok[r] of the concatenated token / cache arrays.
 // K/V cache of one layer: [n_kv][cache_rows][head_dim], cache_rows = total
 // positions of the batch.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -454,7 +456,8 @@ __global__ __launch_bounds__(128) void k_attn_combine(const float* __restrict__ 
 
 hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint16_t* vcache,
                           long cache_rows, uint16_t* o, const WdStepGeom& g, int n_heads, int n_kv,
-                          int head_dim, float* part, long part_floats, hipStream_t st) {
+                          int head_dim, float* part, long part_floats, hipStream_t st,
+                          hipEvent_t e0, hipEvent_t e1) {
   if (head_dim != kAttD) return hipErrorInvalidValue;
   int nqmax = 0, cmax = 0, M = 0;
   long qblocks = 0;
@@ -474,6 +477,16 @@ hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint1
   nsplit = (tiles + tps - 1) / tps;
   float* ml = part + (long)nsplit * M * n_heads * kAttD;
   dim3 grid(n_heads, g.batch, ((nqmax + 63) / 64) * nsplit);
+  // with events, e0 is recorded by the first launch's dispatch and e1 by the last one's
+  if (e0) {
+    hipExtLaunchKernelGGL(k_attn_bf16, grid, dim3(256), 0, st, e0, nsplit > 1 ? nullptr : e1, 0, q,
+                          kcache, vcache, cache_rows, o, g, n_heads, n_kv, nsplit, tps * kKT, M,
+                          part, ml);
+    if (nsplit > 1)
+      hipExtLaunchKernelGGL(k_attn_combine, dim3(M, n_heads), dim3(kAttD), 0, st, nullptr, e1, 0,
+                            (const float*)part, (const float*)ml, nsplit, M, n_heads, o);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_attn_bf16, grid, dim3(256), 0, st, q, kcache, vcache, cache_rows, o, g,
                      n_heads, n_kv, nsplit, tps * kKT, M, part, ml);
   if (nsplit > 1)

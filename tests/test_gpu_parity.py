@@ -201,12 +201,26 @@ def test_profile_records_by_kernel_class():
     n_rows, ms_rows, by_rows, _ = wd.wd_profile_read(m, wd.WD_PROF_GEMM_ROWS)
     n_tiled, ms_tiled, by_tiled, _ = wd.wd_profile_read(m, wd.WD_PROF_GEMM_TILED)
     n_f32 = wd.wd_profile_read(m, wd.WD_PROF_GEMM_F32)[0]
+    n_attn, ms_attn, by_attn, fl_attn = wd.wd_profile_read(m, wd.WD_PROF_ATTN)
     assert n_rows > 0 and n_tiled > 0 and n_f32 == 0
-    assert n_all == n_rows + n_tiled
-    assert ms_all > 0 and abs(ms_all - ms_rows - ms_tiled) <= 1e-6 * ms_all
-    assert abs(by_all - by_rows - by_tiled) <= 1e-9 * by_all
+    assert n_all == n_rows + n_tiled + n_attn
+    assert ms_all > 0 and abs(ms_all - ms_rows - ms_tiled - ms_attn) <= 1e-6 * ms_all
+    assert abs(by_all - by_rows - by_tiled - by_attn) <= 1e-9 * by_all
     # one refresh step: 4 projections per layer through the tiled kernel
     assert n_tiled == 4 * shape.n_layers
+    # attention: one unit per layer and step; K/V of [0, c) plus q and output rows
+    assert n_attn == 4 * shape.n_layers and ms_attn > 0
+    wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
+    want_by = want_fl = 0.0
+    for p in prompts:
+        plan = wd.wd_plan(len(p), 16, wc)
+        for t in range(4):
+            c, r = int(plan["ctx_len"][t]), int(plan["n_rows"][t])
+            want_by += 2.0 * c * shape.n_kv_heads * shape.head_dim * 2
+            want_by += 2.0 * r * shape.n_heads * shape.head_dim * 2
+            want_fl += 4.0 * r * c * shape.n_heads * shape.head_dim
+    assert by_attn == pytest.approx(want_by * shape.n_layers, rel=1e-12)
+    assert fl_attn == pytest.approx(want_fl * shape.n_layers, rel=1e-12)
     # reading does not consume the records; enabling again discards them
     assert wd.wd_profile_read(m, wd.WD_PROF_ALL)[0] == n_all
     wd.wd_profile_enable(m, True)
