@@ -13,8 +13,8 @@ decoded.  `value` is denoising steps per second over the timed generations.
 Also reported: decoded tokens/s, the speedup over standard full-sequence
 decoding on the same GPU and kernels, the roofline of the dominant kernel
 (the few-row projection GEMM of the normal steps, k_gemm_bf16, timed with HIP
-events on the library's stream; HBM bound), the same for the 128-row-tile GEMM
-of the refresh steps (k_gemm_bf16_big; MFMA bound), adaptive termination at
+events on the library's stream; HBM bound), the same for the many-row GEMM
+of the refresh steps (k_gemm_bf16_dma; MFMA bound), adaptive termination at
 <eos> on the same workload (an <eos> id taken from the fixed-length run), the
 buffer-only refresh variant (not the paper's method), the FP8-weight variant
 (not the paper's precision) and the CPU oracle on a bounded sample of the same
@@ -48,7 +48,7 @@ def gemm_source_hash() -> str:
 
 
 # GEMM kernel classes of wd_profile_read and the kernel each one is
-KERNEL_CLASSES = {1: "k_gemm_bf16", 2: "k_gemm_bf16_big"}
+KERNEL_CLASSES = {1: "k_gemm_bf16", 2: "k_gemm_bf16_dma"}
 PROFILE_NAMES = {**KERNEL_CLASSES, 4: "k_attn_bf16"}
 
 
@@ -67,8 +67,9 @@ def measured_traffic(kernel: str):
 def kernel_class_of(name: str):
     """WD_PROF_* class of a kernel name as rocprofv3 prints it: the few-row
     products (k_gemm_bf16, and k_gemm_bf16_fused that carries the Q/K/V or
-    SwiGLU epilogue) or the 128-row-tile kernel."""
-    if "k_gemm_bf16_big<" in name:
+    SwiGLU epilogue) or the many-row kernels (k_gemm_bf16_dma; k_gemm_bf16_big
+    where the former does not apply: fp8 weights, widths not a multiple of 256)."""
+    if "k_gemm_bf16_dma<" in name or "k_gemm_bf16_big<" in name:
         return 2
     if "k_gemm_bf16<" in name or "k_gemm_bf16_fused<" in name:
         return 1
@@ -143,7 +144,7 @@ def pmc_summary(gemm_fetch: str, gemm_write: str, copy_fetch: str, copy_write: s
 def roofline_of(model, kernel_class: int, elapsed_ev: float):
     """Roofline entry of one GEMM kernel from the event-timed launches of the
     instrumented pass: the few-row kernel streams its weights (HBM bound), the
-    128-row-tile kernel is priced against dense bf16 MFMA."""
+    many-row kernel is priced against dense bf16 MFMA."""
     import paper_2601_20332_amd as wd
     launches, ms, alg_bytes, alg_flops = wd.wd_profile_read(model, kernel_class)
     if launches <= 0 or ms <= 0:
@@ -154,7 +155,7 @@ def roofline_of(model, kernel_class: int, elapsed_ev: float):
     tfs = alg_flops / launches / avg_s / 1e12
     hbm = kernel_class in (1, 4)
     achieved, peak = (gbs, HBM_PEAK_GBS) if hbm else (tfs, BF16_PEAK_TFLOPS)
-    label = {1: " + k_gemm_bf16_fused (at most 64 rows)", 2: " (128-row tiles)",
+    label = {1: " + k_gemm_bf16_fused (at most 64 rows)", 2: " (more than 64 rows)",
              4: " + k_attn_combine (one layer's attention)"}[kernel_class]
     return {
         "kernel": name + label,
@@ -544,7 +545,7 @@ def main():
         elapsed_ev = time.perf_counter() - t_ev
         # the dominant kernel: few-row weight-streaming GEMM of the normal steps
         roofline = roofline_of(model, wd.WD_PROF_GEMM_ROWS, elapsed_ev)
-        # second: the 128-row-tile GEMM of the refresh steps
+        # second: the many-row GEMM of the refresh steps
         roofline_tiled = roofline_of(model, wd.WD_PROF_GEMM_TILED, elapsed_ev)
         # attention: K/V of [0, c) streamed per layer and step
         roofline_attn = roofline_of(model, wd.WD_PROF_ATTN, elapsed_ev)

@@ -284,8 +284,9 @@ enum {
   WD_PROF_ALL = 0,        /* every recorded launch */
   WD_PROF_GEMM_ROWS = 1,  /* k_gemm_bf16: at most 64 rows, each weight read once (normal
                              steps, LM head) */
-  WD_PROF_GEMM_TILED = 2, /* k_gemm_bf16_big: more than 64 rows in 128-row tiles (refresh
-                             and full-sequence steps) */
+  WD_PROF_GEMM_TILED = 2, /* more than 64 rows (refresh and full-sequence steps):
+                             k_gemm_bf16_dma (bf16, widths a multiple of 256), else
+                             k_gemm_bf16_big */
   WD_PROF_GEMM_F32 = 3,   /* k_gemm_f32: fp32 models */
   WD_PROF_ATTN = 4        /* bf16 attention of one layer (k_attn_bf16 and, when the keys are
                              split, k_attn_combine, timed as one unit); bytes = K and V rows

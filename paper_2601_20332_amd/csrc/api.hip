@@ -661,7 +661,7 @@ struct SeqLayout {
 
 int gemm_splits(const wd_model_config& c, int M, int N, int K) {
   if (c.dtype != WD_DTYPE_BF16) return 1;
-  return wd::plan_gemm_bf16(M, N, K).splits;
+  return wd::plan_gemm_bf16(M, N, K, c.weight_fp8 != 0).splits;
 }
 
 SeqLayout seq_layout(const wd_model& m, const wd_window_config& w, int B, long T, int Smax, int G) {
@@ -854,12 +854,7 @@ wd_status gemm_launch(wd_seq* s, const T* X, int ldx, const void* W, const float
                       hipEvent_t e1) {
   const wd_model& m = *s->m;
   if (m.cfg.dtype == WD_DTYPE_BF16) {
-    wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K, wsc != nullptr);
-    if (p.splits > max_splits) {
-      p.splits = 1;
-      p.ks_per_split = K / 32;
-      p.grid = (N / (64 * p.nf)) * ((M + 16 * p.mf - 1) / (16 * p.mf));
-    }
+    const wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K, wsc != nullptr, max_splits);
     if ((size_t)p.splits * M * N > s->C_floats && C == s->C)
       return fail(WD_ERR_DEVICE, "internal: partial buffer too small");
     WD_HIP(wd::gemm_bf16((const uint16_t*)X, ldx, W, C, M, N, K, p, m.stream, e0, e1, wsc));

@@ -12,6 +12,7 @@
 // launch has enough workgroups to keep every CU's memory pipeline full.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <climits>
 #include <type_traits>
 
@@ -868,9 +869,207 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
 // full-sequence path, batches): 128-row tiles, 2 weight groups per wave,
 // software-pipelined, K splits until 256 workgroups run (split-K partials
 // cost rows*N*4 bytes each).
-GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8) {
+// ---- bf16 GEMM for many rows: multi-stage LDS pipeline fed by direct-to-LDS loads -------
+// Workgroup tile: 64 * MFW rows x 256 features; wave (wm, wn) computes
+// 32 * MFW rows x 128 features on v_mfma_f32_32x32x16_bf16 (weights as the
+// A operand, activations as B), accumulators in AGPRs.  Each 32-wide K step
+// is one stage in LDS, filled by 16-byte direct-to-LDS loads (lane l of a
+// load lands at +16 l) ST - 1 stages ahead of the step being computed; one
+// barrier per stage, with the waits issued by hand so that the compiler does
+// not drain every load at the barrier.
+// Stage layout (1 KB blocks after a 1 KB pad that keeps every load target off
+// LDS address 0):
+//   activation blocks 0 .. 4 MFW - 1: tile rows 16 b .. 16 b + 15, 64 bytes
+//     each; the 16-byte chunk c of row r sits in slot c ^ swz(r), with
+//     swz(r) = ((r >> 1) ^ (r >> 2)) & 3, so the 32-row operand reads hit
+//     distinct banks;
+//   weight blocks 4 MFW + 2 i + h: the A operand of feature block i (packed
+//     groups 2 i, 2 i + 1 of the tile) for K half h, assembled by the loads
+//     themselves from the two packed 16x32 fragments: rows of 16 lanes
+//     [g0 h0 g1 h1] (h = 0) and [g2 h2 g3 h3] (h = 1).
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+// at most N vector-memory operations of this wave outstanding (vmcnt in bits
+// 3:0 and 15:14; expcnt and lgkmcnt left unconstrained)
+#define WD_WAIT_VM(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | 0x70 | 0xF00 | ((((N) >> 4) & 3) << 14))
+// every LDS operation of this wave complete (lgkmcnt 0; vmcnt, expcnt free)
+#define WD_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xC07F)
+
+template <int MFW, int ST>
+__global__ __launch_bounds__(256, 1) void k_gemm_bf16_dma(const uint16_t* __restrict__ X, int ldx,
+                                                          const u32x4* __restrict__ Wp,
+                                                          float* __restrict__ C, int M, int N,
+                                                          int K, int NB, int MT, int S, int ks) {
+  // the host pass only needs the kernel's signature
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int NFW = 4;
+  constexpr int F = 4 * (MFW + NFW);     // 1 KB blocks per stage
+  constexpr int FW = MFW + NFW;          // blocks each wave loads per stage
+  constexpr int STAGE16 = (F + 1) * 64;  // u32x4 per stage buffer, pad included
+  static_assert(ST >= 3 && ST <= 4, "stages");
+  static_assert((ST - 2) * FW < 64, "outstanding loads fit the wait counter");
+  __shared__ __attribute__((aligned(16))) u32x4 st0[STAGE16], st1[STAGE16], st2[STAGE16],
+      st3[ST > 3 ? STAGE16 : 1];
+  const int G = NB * MT * S;
+  int id = blockIdx.x;
+  if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);
+  const int mt = id % MT, rest = id / MT, nb = rest % NB, sp = rest / NB;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int KT = K >> 5;
+  const int kt0 = sp * ks, nkt = min(KT, kt0 + ks) - kt0;
+  const int m0 = mt * 64 * MFW;
+  // per-lane source of every block this wave loads, at K step kt0
+  const u32x4* src[FW];
+  int step16[FW];  // u32x4 between consecutive K steps
+#pragma unroll
+  for (int q = 0; q < FW; ++q) {
+    const int f = wave + 4 * q;
+    if (f < 4 * MFW) {
+      const int r = f * 16 + (lane >> 2);
+      const int c = (lane & 3) ^ (((r >> 1) ^ (r >> 2)) & 3);
+      const long row = min(m0 + r, M - 1);
+      src[q] = (const u32x4*)(X + row * ldx + kt0 * 32 + c * 8);
+      step16[q] = 4;
+    } else {
+      const int i = (f - 4 * MFW) >> 1, h = f & 1;
+      const int g = 2 * (nb * 2 * NFW + i) + ((lane >> 4) & 1);
+      const int sl = (lane & 15) + 16 * (2 * h + (lane >> 5));
+      src[q] = Wp + ((long)g * KT + kt0) * 64 + sl;
+      step16[q] = 64;
+    }
+  }
+  auto stage = [&](auto B) -> u32x4* {
+    constexpr int b = decltype(B)::value;
+    if constexpr (b == 0) return st0 + 64;
+    else if constexpr (b == 1) return st1 + 64;
+    else if constexpr (b == 2) return st2 + 64;
+    else return st3 + 64;
+  };
+  auto issue = [&](auto B, int it) {
+    const int k = min(it, nkt - 1);  // steps past the split reload its last one, unused
+    u32x4* dst = stage(B);
+#pragma unroll
+    for (int q = 0; q < FW; ++q)
+      __builtin_amdgcn_global_load_lds(src[q] + (long)k * step16[q], dst + (wave + 4 * q) * 64, 16,
+                                       0, 0);
+  };
+  f32x16 acc[NFW][MFW];
+#pragma unroll
+  for (int a = 0; a < NFW; ++a)
+#pragma unroll
+    for (int b = 0; b < MFW; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
+  auto compute = [&](auto B) {
+    const u32x4* sb = stage(B);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      u32x4 a[NFW], bx[MFW];
+#pragma unroll
+      for (int ii = 0; ii < NFW; ++ii) a[ii] = sb[(4 * MFW + 2 * (wn * NFW + ii) + h) * 64 + lane];
+#pragma unroll
+      for (int jj = 0; jj < MFW; ++jj) {
+        const int r = (wm * MFW + jj) * 32 + (lane & 31);
+        const int slot = (2 * h + (lane >> 5)) ^ (((r >> 1) ^ (r >> 2)) & 3);
+        bx[jj] = sb[r * 4 + slot];
+      }
+#pragma unroll
+      for (int jj = 0; jj < MFW; ++jj)
+#pragma unroll
+        for (int ii = 0; ii < NFW; ++ii) acc[ii][jj] = mfma32(a[ii], bx[jj], acc[ii][jj]);
+    }
+  };
+  // step it: its loads are done (this wave: at most the later stages' loads
+  // outstanding; every wave: the barrier), every wave has finished reading the
+  // buffer of step it - 1, which is refilled with step it + ST - 1
+  auto body = [&](auto J, int it) {
+    constexpr int j = decltype(J)::value;
+    WD_WAIT_VM((ST - 2) * FW);
+    WD_WAIT_LGKM0();
+    __builtin_amdgcn_s_barrier();
+    issue(ic<(j + ST - 1) % ST>{}, it + ST - 1);
+    if (it < nkt) compute(ic<j % ST>{});
+  };
+  issue(ic<0>{}, 0);
+  issue(ic<1>{}, 1);
+  if constexpr (ST > 3) issue(ic<2>{}, 2);
+  for (int it = 0; it < nkt; it += ST) {
+    body(ic<0>{}, it);
+    body(ic<1>{}, it + 1);
+    body(ic<2>{}, it + 2);
+    if constexpr (ST > 3) body(ic<3>{}, it + 3);
+  }
+  WD_WAIT_VM(0);  // no load may land in LDS after the workgroup ends
+  // D of (feature block i, row block j): lane l holds row j * 32 + l % 32,
+  // features i * 32 + (e / 4) * 8 + (l / 32) * 4 + e % 4
+#pragma unroll
+  for (int ii = 0; ii < NFW; ++ii)
+#pragma unroll
+    for (int jj = 0; jj < MFW; ++jj) {
+      const int m = m0 + (wm * MFW + jj) * 32 + (lane & 31);
+      if (m >= M) continue;
+      const int n0 = (nb * 2 * NFW + wn * NFW + ii) * 32 + (lane >> 5) * 4;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 v = {acc[ii][jj][g * 4], acc[ii][jj][g * 4 + 1], acc[ii][jj][g * 4 + 2],
+                         acc[ii][jj][g * 4 + 3]};
+        *(f32x4*)(C + ((long)sp * M + m) * N + n0 + g * 8) = v;
+      }
+    }
+#endif
+}
+
+GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
   GemmPlan p;
   const int KT = K / 32;
+  if (M > 64 && !w8 && N % 256 == 0) {
+    // k_gemm_bf16_dma: 64 * mfw-row x 256-feature tiles, S K splits.  Measured
+    // on the projection shapes (224 to 600 rows): a grid that fits one round of
+    // one workgroup per CU (128 to 256 workgroups) beats more, smaller
+    // workgroups, and partials cost their epilogue a read each.  So: a
+    // one-round grid if there is one, else no K split if the tiles alone give
+    // 256 workgroups; then least work per CU (rounds x rows x K steps), at
+    // least 32 K steps per split, taller tiles, fewer splits.
+    struct Cand {
+      int mfw, splits, ks;
+      long grid, key[5];
+    };
+    Cand c[8];
+    int n = 0;
+    bool one_round = false, unsplit_fills = false;
+    for (int mfw : {4, 2})
+      for (int S = 1; S <= 8 && S <= max_splits; S *= 2) {
+        const int ks = (KT + S - 1) / S;
+        if (S > 1 && ks < 8) break;
+        const int splits = (KT + ks - 1) / ks;
+        const int MT = (M + 64 * mfw - 1) / (64 * mfw);
+        const long grid = (long)(N / 256) * MT * splits;
+        const long rounds = (grid + 255) / 256;
+        const bool single = grid >= 128 && rounds == 1;
+        one_round |= single;
+        unsplit_fills |= splits == 1 && grid >= 256;
+        c[n++] = {mfw, splits, ks, grid,
+                  {single ? 0 : 1, rounds * mfw * ks, ks >= 32 ? 0 : 1, -mfw, splits}};
+      }
+    const Cand* pick = nullptr;
+    for (int i = 0; i < n; ++i) {
+      if (!one_round && unsplit_fills && c[i].splits != 1) continue;
+      if (!pick || std::lexicographical_compare(c[i].key, c[i].key + 5, pick->key, pick->key + 5))
+        pick = &c[i];
+    }
+    p.dma_mfw = pick->mfw;
+    p.splits = pick->splits;
+    p.ks_per_split = pick->ks;
+    p.grid = (int)pick->grid;
+    p.mf = 8;
+    p.nf = 4;
+    p.ck = 1;
+    return p;
+  }
   if (M <= 64) {
     p.nf = (N >= 16384 && N % 128 == 0) ? 2 : 1;
     p.mf = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
@@ -884,7 +1083,7 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8) {
   const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
   const long target = M > 64 ? 256 : p.nf == 2 ? 384 : 512;
   int S = 1;
-  while ((long)NB * MT * S < target && KT / (2 * S) >= p.ck) S *= 2;
+  while ((long)NB * MT * S < target && KT / (2 * S) >= p.ck && 2 * S <= max_splits) S *= 2;
   p.ks_per_split = (KT + S - 1) / S;
   if (w8) p.ks_per_split += p.ks_per_split & 1;  // fp8 fragments hold K steps in pairs
   p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
@@ -915,6 +1114,23 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
                      const GemmPlan& p, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
                      const float* wsc) {
   if (M <= 0) return hipSuccess;
+  if (p.dma_mfw) {
+    const int NB = N / 256, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
+    const int KT = K / 32;
+    if (wsc || N % 256 || K % 32 || NB * MT * p.splits != p.grid || p.ks_per_split <= 0 ||
+        (long)p.ks_per_split * p.splits < KT || (long)p.ks_per_split * (p.splits - 1) >= KT)
+      return hipErrorInvalidValue;
+    const dim3 grid(p.grid);
+    if (p.dma_mfw == 4)
+      launch_timed(k_gemm_bf16_dma<4, 3>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
+                   M, N, K, NB, MT, p.splits, p.ks_per_split);
+    else if (p.dma_mfw == 2)
+      launch_timed(k_gemm_bf16_dma<2, 4>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
+                   M, N, K, NB, MT, p.splits, p.ks_per_split);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   const int NB = N / (16 * kWaves * p.nf);
   const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
   if (NB * MT * p.splits != p.grid || N % (16 * kWaves * p.nf) || K % 32) return hipErrorInvalidValue;

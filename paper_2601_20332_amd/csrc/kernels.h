@@ -19,8 +19,10 @@ struct GemmPlan {
   int splits = 1;        // K splits = number of partial outputs
   int ks_per_split = 0;  // 32-wide K steps per split
   int grid = 0;
+  int dma_mfw = 0;       // > 0: k_gemm_bf16_dma with 64 * dma_mfw-row tiles
 };
-GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8 = false);
+// Launch plan for C = X W^T; at most max_splits K splits.
+GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8 = false, int max_splits = 1 << 20);
 // Row orders of packed weights (gemm.hip): plain; RoPE pairs adjacent within
 // each 128-row head (Q/K/V); gate and up interleaved by 8 rows (W2 = up).
 constexpr int kPackPlain = 0, kPackRopePair = 1, kPackGateUp = 2;
