@@ -477,6 +477,25 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
     xstore(ic<(j + 1) % XD>{}, (j + 1) & 1, it + 1);
     __syncthreads();
   };
+  // Q/K/V epilogue inputs, loaded before the K loop so that their latency
+  // (the cos/sin address depends on the row's position) hides behind it
+  [[maybe_unused]] float qkv_bias[4];
+  [[maybe_unused]] f32x4 qkv_cs[MF][2];
+  [[maybe_unused]] int qkv_tok[MF];
+  if constexpr (EPI == kEpiQkv) {
+    const int head = grp >> 3, i0 = (grp & 7) * 8 + ((lane >> 4) & 1) * 4;
+    const int dim0 = (lane >> 5) * 64 + i0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) qkv_bias[j] = ep.bias ? bf2f(ep.bias[head * 128 + dim0 + j]) : 0.f;
+#pragma unroll
+    for (int jf = 0; jf < MF; ++jf) {
+      const int m = min(jf * 16 + (lane & 15), M - 1);
+      qkv_tok[jf] = ep.row_tok[m];
+      const f32x4* cs = (const f32x4*)(ep.rope_cs + ((long)ep.row_pos[m] * 64 + i0) * 2);
+      qkv_cs[jf][0] = cs[0];
+      qkv_cs[jf][1] = cs[1];
+    }
+  }
   xload(ic<0>{}, 0);
   xload(ic<1>{}, 1);
   wload(ic<0>{}, 0);
@@ -505,24 +524,20 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
     const int i0 = gi * 8 + sub;          // rotation index of j = 0 (< 64)
     const int dim0 = hi * 64 + i0;        // this lane's dims dim0 .. dim0 + 3
     const bool rot = head < ep.nh + ep.nkv;
-    float bias[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) bias[j] = ep.bias ? bf2f(ep.bias[head * 128 + dim0 + j]) : 0.f;
 #pragma unroll
     for (int jf = 0; jf < MF; ++jf) {
       float x[4], p[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[j] = acc[jf][j] + bias[j];
+        x[j] = acc[jf][j] + qkv_bias[j];
         p[j] = __shfl_xor(x[j], 32, 64);
       }
       const int m = jf * 16 + (lane & 15);
       if (m >= M) continue;
       if (rot) {
-        const float* cs = ep.rope_cs + ((long)ep.row_pos[m] * 64 + i0) * 2;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float c = cs[2 * j], sn = cs[2 * j + 1];
+          const float c = qkv_cs[jf][j >> 1][(j & 1) * 2], sn = qkv_cs[jf][j >> 1][(j & 1) * 2 + 1];
           x[j] = hi ? x[j] * c + p[j] * sn : x[j] * c - p[j] * sn;
         }
       }
@@ -530,9 +545,9 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
       if (head < ep.nh)
         dst = ep.q + ((long)m * ep.nh + head) * 128;
       else if (head < ep.nh + ep.nkv)
-        dst = ep.kc + ((long)(head - ep.nh) * ep.cache_rows + ep.row_tok[m]) * 128;
+        dst = ep.kc + ((long)(head - ep.nh) * ep.cache_rows + qkv_tok[jf]) * 128;
       else
-        dst = ep.vc + ((long)(head - ep.nh - ep.nkv) * ep.cache_rows + ep.row_tok[m]) * 128;
+        dst = ep.vc + ((long)(head - ep.nh - ep.nkv) * ep.cache_rows + qkv_tok[jf]) * 128;
       u32x2 w;
       w.x = (uint32_t)f2bf(x[0]) | ((uint32_t)f2bf(x[1]) << 16);
       w.y = (uint32_t)f2bf(x[2]) | ((uint32_t)f2bf(x[3]) << 16);
