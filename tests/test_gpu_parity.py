@@ -83,6 +83,19 @@ def test_bf16_gqa_bias_batched():
     _run_and_check(MICRO_GQA, prompts, 30, synth.WindowSettings(6, 10, 3, 2))
 
 
+# widths that are not multiples of 256 (hidden 384: Q/K/V 1152, O and down 384)
+# take the 128-row-tile fallback above 64 rows; gate/up (1280) the LDS-pipelined
+# tiles; rows 65-170 cover one and two row tiles and short K splits
+MICRO_ODD = synth.ModelShape(n_layers=2, hidden=384, n_heads=3, n_kv_heads=3, head_dim=128,
+                             ffn=640, vocab=1536, dtype=synth.DTYPE_BF16, rms_eps=1e-5,
+                             rope_theta=10000.0)
+
+
+def test_bf16_many_row_kernels_odd_widths():
+    prompts = synth.prompts(MICRO_ODD, [65, 100])
+    _run_and_check(MICRO_ODD, prompts, 40, synth.WindowSettings(8, 24, 4, 2))
+
+
 def test_bf16_full_sequence_path():
     prompts = synth.prompts(MICRO_GQA, [20, 9])
     _run_and_check(MICRO_GQA, prompts, 12, synth.WindowSettings(4, 4, 2, 2), full=True)
