@@ -979,19 +979,26 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16_dma(const uint16_t* __rest
     for (int b = 0; b < MFW; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
+  // Per-lane offsets (u32x4) of this wave's operands inside a stage: weight
+  // block 4 MFW + 2 (wn NFW + ii) + h, and activation row (wm MFW + jj) 32 +
+  // l % 32 in slot (2 h + l / 32) ^ swz(l) (swz only sees the row's low bits).
+  // They are kept opaque so that each operand read is its stage buffer plus
+  // one offset and a constant: the LDS lowering tags an access with its buffer
+  // only a few address steps deep, and for an untagged read the compiler
+  // waits for every direct-to-LDS load in flight.
+  int a_off = (4 * MFW + 2 * wn * NFW) * 64 + lane;
+  int x_off0 = wm * MFW * 128 + (lane & 31) * 4 + (((lane >> 5) ^ (lane >> 1) ^ (lane >> 2)) & 3);
+  int x_off1 = wm * MFW * 128 + (lane & 31) * 4 + ((2 + (lane >> 5)) ^ (((lane >> 1) ^ (lane >> 2)) & 3));
+  asm volatile("" : "+v"(a_off), "+v"(x_off0), "+v"(x_off1));
   auto compute = [&](auto B) {
     const u32x4* sb = stage(B);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       u32x4 a[NFW], bx[MFW];
 #pragma unroll
-      for (int ii = 0; ii < NFW; ++ii) a[ii] = sb[(4 * MFW + 2 * (wn * NFW + ii) + h) * 64 + lane];
+      for (int ii = 0; ii < NFW; ++ii) a[ii] = sb[a_off + ii * 128 + h * 64];
 #pragma unroll
-      for (int jj = 0; jj < MFW; ++jj) {
-        const int r = (wm * MFW + jj) * 32 + (lane & 31);
-        const int slot = (2 * h + (lane >> 5)) ^ (((r >> 1) ^ (r >> 2)) & 3);
-        bx[jj] = sb[r * 4 + slot];
-      }
+      for (int jj = 0; jj < MFW; ++jj) bx[jj] = sb[(h ? x_off1 : x_off0) + jj * 128];
 #pragma unroll
       for (int jj = 0; jj < MFW; ++jj)
 #pragma unroll
@@ -1053,10 +1060,10 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
       int mfw, splits, ks;
       long grid, key[5];
     };
-    Cand c[8];
+    Cand c[12];
     int n = 0;
     bool one_round = false, unsplit_fills = false;
-    for (int mfw : {4, 2})
+    for (int mfw : {4, 3, 2})
       for (int S = 1; S <= 8 && S <= max_splits; S *= 2) {
         const int ks = (KT + S - 1) / S;
         if (S > 1 && ks < 8) break;
@@ -1138,6 +1145,9 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
     const dim3 grid(p.grid);
     if (p.dma_mfw == 4)
       launch_timed(k_gemm_bf16_dma<4, 3>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
+                   M, N, K, NB, MT, p.splits, p.ks_per_split);
+    else if (p.dma_mfw == 3)
+      launch_timed(k_gemm_bf16_dma<3, 4>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
                    M, N, K, NB, MT, p.splits, p.ks_per_split);
     else if (p.dma_mfw == 2)
       launch_timed(k_gemm_bf16_dma<2, 4>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
