@@ -384,15 +384,25 @@ struct FusedEpi {
 template <int V>
 using ic = std::integral_constant<int, V>;
 
-template <int EPI, int MF, int U, bool W8, int GW>
+// f(ic<I>{}), f(ic<I + 1>{}), ..., f(ic<N - 1>{})
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(ic<I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+// R: depth of the weight ring (loads run R - 1 iterations ahead); XD: the
+// activations are loaded XD iterations ahead and staged in LDS one ahead.
+template <int EPI, int MF, int U, bool W8, int GW, int R, int XD>
 __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __restrict__ X, int ldx,
                                                              const u32x4* __restrict__ Wp, int M,
                                                              int N, int K, FusedEpi ep,
                                                              const float* __restrict__ wsc) {
   static_assert(EPI != kEpiConf || GW == kWaves, "the confidence epilogue reduces 64-entry tiles");
+  static_assert(R % XD == 0 && XD % 2 == 0, "ring slots and activation buffers repeat together");
   constexpr int NT = 64 * GW;
-  constexpr int R = 4;   // weight ring: loads run R - 1 iterations ahead
-  constexpr int XD = 2;  // activations: loaded XD iterations ahead, staged one ahead
   constexpr int ROWS = 16 * MF;
   constexpr int PITCH = U * 32 + 8;
   constexpr int CHUNK16 = ROWS * U * 4;
@@ -496,19 +506,12 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
       qkv_cs[jf][1] = cs[1];
     }
   }
-  xload(ic<0>{}, 0);
-  xload(ic<1>{}, 1);
-  wload(ic<0>{}, 0);
-  wload(ic<1>{}, 1);
-  wload(ic<2>{}, 2);
+  static_for<0, XD>([&](auto J) { xload(J, decltype(J)::value); });
+  static_for<0, R - 1>([&](auto J) { wload(J, decltype(J)::value); });
   xstore(ic<0>{}, 0, 0);
   __syncthreads();
-  for (int it = 0; it < n_it; it += R) {
-    body(ic<0>{}, it);
-    body(ic<1>{}, it + 1);
-    body(ic<2>{}, it + 2);
-    body(ic<3>{}, it + 3);
-  }
+  for (int it = 0; it < n_it; it += R)
+    static_for<0, R>([&](auto J) { body(J, it + decltype(J)::value); });
 
   // lane l holds packed rows grp*16 + (l/16)*4 + j (j < 4) of activation rows
   // j*16 + l%16; packed rows 0..7 of a group pair with rows 8..15 (lane l ^ 32)
@@ -644,47 +647,73 @@ bool fused_rows_ok(int M, int N, int K) {
   return M >= 1 && M <= 64 && N % 64 == 0 && K % 32 == 0 && N / 64 >= 192;
 }
 
-template <int EPI, int U, bool W8, int GW>
+template <int EPI, int U, bool W8, int GW, int R, int XD = 2>
 static void launch_fused_mf(dim3 grid, int M, const uint16_t* X, int ldx, const u32x4* W, int N,
                             int K, const FusedEpi& ep, const float* wsc, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1) {
   const dim3 block(64 * GW);
   switch ((M + 15) / 16) {
-    case 1: launch_timed_block(k_gemm_bf16_fused<EPI, 1, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
-    case 2: launch_timed_block(k_gemm_bf16_fused<EPI, 2, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
-    case 3: launch_timed_block(k_gemm_bf16_fused<EPI, 3, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
-    default: launch_timed_block(k_gemm_bf16_fused<EPI, 4, U, W8, GW>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 1: launch_timed_block(k_gemm_bf16_fused<EPI, 1, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 2: launch_timed_block(k_gemm_bf16_fused<EPI, 2, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 3: launch_timed_block(k_gemm_bf16_fused<EPI, 3, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    default: launch_timed_block(k_gemm_bf16_fused<EPI, 4, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
   }
 }
 
-// GW weight groups (16 features each) per workgroup, one wave each: 4 by
-// default; 6 when that gives at least one workgroup per CU, which spreads a
-// wide matrix (gate/up) evenly over the 256 CUs instead of 1.5 workgroups per CU.
+// GW weight groups (16 features each) per workgroup, one wave each.  A wave
+// streams at a bounded rate (its loop is latency-bound with one wave per
+// SIMD), so a launch is fastest when its workgroups fill the 256 CUs in as
+// few rounds as possible: the least rounds x GW, ties to more groups per
+// workgroup (every workgroup stages all activation rows).  Two groups only
+// when that is still one round.  Measured (33-39 rows): Q/K/V 4096 x 12288
+// 20.1 us with GW 3 against 21.2 with GW 4; 3584 x 4608 15.5 with GW 2
+// against 17.1; gate/up 4096 x 24576 33.7 with GW 6 against 38.9 with GW 4.
+// The LM head's confidence epilogue needs GW 4.
+static int fused_groups_per_wg(int groups) {
+  int best = 4;
+  long best_key = LONG_MAX;
+  for (int gw : {6, 4, 3, 2}) {
+    if (groups % gw) continue;
+    const long wgs = groups / gw, rounds = (wgs + 255) / 256;
+    if (gw == 2 && rounds > 1) continue;
+    const long key = rounds * gw * 8 + (8 - gw);
+    if (key < best_key) {
+      best_key = key;
+      best = gw;
+    }
+  }
+  return best;
+}
+
+template <int EPI, int U, bool W8>
+static void launch_fused_gw(int gw, const uint16_t* X, int ldx, const u32x4* W, int M, int N,
+                            int K, const FusedEpi& ep, const float* wsc, hipStream_t st,
+                            hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid(N / 16 / gw);
+  if constexpr (EPI == kEpiConf) {
+    launch_fused_mf<EPI, U, W8, 4, 4, 2>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
+  } else {
+    switch (gw) {
+      case 6: launch_fused_mf<EPI, U, W8, 6, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
+      case 3: launch_fused_mf<EPI, U, W8, 3, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
+      case 2: launch_fused_mf<EPI, U, W8, 2, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
+      default: launch_fused_mf<EPI, U, W8, 4, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
+    }
+  }
+}
+
 template <int EPI, int U>
 static hipError_t launch_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
                                const FusedEpi& ep, const float* wsc, hipStream_t st, hipEvent_t e0,
                                hipEvent_t e1) {
   if (!fused_rows_ok(M, N, K) || (wsc && K % 64)) return hipErrorInvalidValue;
   const u32x4* W = (const u32x4*)Wp;
-  const int groups = N / 16;
-  bool six = false;
-  if constexpr (EPI != kEpiConf) {
-    six = groups % 6 == 0 && groups / 6 >= 256;
-    if (six) {
-      const dim3 grid(groups / 6);
-      if (wsc)
-        launch_fused_mf<EPI, U, true, 6>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
-      else
-        launch_fused_mf<EPI, U, false, 6>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
-    }
-  }
-  if (!six) {
-    const dim3 grid(groups / 4);
-    if (wsc)
-      launch_fused_mf<EPI, U, true, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
-    else
-      launch_fused_mf<EPI, U, false, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
-  }
+  const int gw = EPI == kEpiConf ? 4 : fused_groups_per_wg(N / 16);
+  if ((N / 16) % gw) return hipErrorInvalidValue;
+  if (wsc)
+    launch_fused_gw<EPI, U, true>(gw, X, ldx, W, M, N, K, ep, wsc, st, e0, e1);
+  else
+    launch_fused_gw<EPI, U, false>(gw, X, ldx, W, M, N, K, ep, wsc, st, e0, e1);
   return hipGetLastError();
 }
 

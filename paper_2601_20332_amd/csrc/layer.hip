@@ -24,7 +24,7 @@ __global__ __launch_bounds__(1024) void k_embed_norm(const int32_t* __restrict__
   const long r = blockIdx.x;
   const T* e = emb + (long)x[row_tok[r]] * H;
   float* hr = h + r * H;
-  float v[4][4];
+  float v[4][4], g[4][4];
   float ss = 0.f;
 #pragma unroll
   for (int it = 0; it < 4; ++it) {
@@ -32,6 +32,7 @@ __global__ __launch_bounds__(1024) void k_embed_norm(const int32_t* __restrict__
     if (i < H) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
+        g[it][q] = Elem<T>::load(gamma + i + q);
         v[it][q] = Elem<T>::load(e + i + q);
         ss += v[it][q] * v[it][q];
       }
@@ -44,8 +45,7 @@ __global__ __launch_bounds__(1024) void k_embed_norm(const int32_t* __restrict__
     const int i = (threadIdx.x + it * 1024) * 4;
     if (i < H)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        a[r * H + i + q] = Elem<T>::from_f(v[it][q] * inv * Elem<T>::load(gamma + i + q));
+      for (int q = 0; q < 4; ++q) a[r * H + i + q] = Elem<T>::from_f(v[it][q] * inv * g[it][q]);
   }
 }
 
@@ -71,11 +71,14 @@ __global__ __launch_bounds__(1024) void k_residual_norm(float* __restrict__ h,
   const long r = blockIdx.x;
   float* hr = h + r * H;
   f32x4 v[4];
+  float g[4][4];  // gains, loaded with the partials rather than after the reduction
   float ss = 0.f;
 #pragma unroll
   for (int it = 0; it < 4; ++it) {
     const int i = (threadIdx.x + it * 1024) * 4;
     if (i < H) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) g[it][q] = Elem<T>::load(gamma + i + q);
       const f32x4 acc = split_sum((const f32x4*)(C + r * H + i), (long)M * H / 4, S);
       v[it] = *(const f32x4*)(hr + i) + acc;
       *(f32x4*)(hr + i) = v[it];
@@ -90,8 +93,7 @@ __global__ __launch_bounds__(1024) void k_residual_norm(float* __restrict__ h,
     const int i = (threadIdx.x + it * 1024) * 4;
     if (i < H)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        a[(long)dst * H + i + q] = Elem<T>::from_f(v[it][q] * inv * Elem<T>::load(gamma + i + q));
+      for (int q = 0; q < 4; ++q) a[(long)dst * H + i + q] = Elem<T>::from_f(v[it][q] * inv * g[it][q]);
   }
 }
 
