@@ -379,6 +379,9 @@ struct FusedEpi {
   float* logits;            // [M][V] fp32, or null
   float *pmax, *psum;       // [M][n_tiles]
   int* pidx;
+  // K-split partials: split s of `splits` covers K steps [s ks, s ks + ks)
+  float* C;                 // [splits][M][N] fp32
+  int splits, ks;
 };
 
 template <int V>
@@ -411,19 +414,24 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
   const int G = gridDim.x;
   int id = blockIdx.x;
   if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);
-  const int nb = id;
+  // with a K split, workgroup id takes group block id % nblk over split id / nblk
+  const int nblk = EPI == kEpiPartial ? G / ep.splits : G;
+  const int nb = id % nblk, sp = id / nblk;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int KT = K >> 5;
+  const int kt_begin = EPI == kEpiPartial ? sp * ep.ks : 0;
+  const int KTs = EPI == kEpiPartial ? min(KT, kt_begin + ep.ks) - kt_begin : KT;  // this split's
   const int grp = nb * GW + wave;  // this wave's 16-row weight group
   // W8: the ring holds raw fp8 fragments (one per two K steps), decoded when used
   constexpr int UW = W8 ? U / 2 : U;
-  const int frags = W8 ? KT / 2 : KT;
-  const u32x4* wp = Wp + (long)grp * frags * 64 + lane;
+  const int frags = W8 ? KTs / 2 : KTs;
+  const u32x4* wp =
+      Wp + ((long)grp * (W8 ? KT / 2 : KT) + (W8 ? kt_begin / 2 : kt_begin)) * 64 + lane;
   f32x4 acc[MF];
 #pragma unroll
   for (int b = 0; b < MF; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
   const u32x4 zero = {0u, 0u, 0u, 0u};
-  const int n_it = (KT + U - 1) / U;
+  const int n_it = (KTs + U - 1) / U;
   u32x4 pre[XD][PER_T];
   u32x4 a[R][UW];
   auto wload = [&](auto B, int it) {
@@ -439,7 +447,7 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
       const int e = min(tid + i * NT, CHUNK16 - 1);
       const int r = e / (U * 4), cc = e % (U * 4);
       const long row = min(r, M - 1);
-      const int kc = min(it * U + cc / 4, KT - 1);
+      const int kc = kt_begin + min(it * U + cc / 4, KTs - 1);
       pre[p][i] = *(const u32x4*)(X + row * ldx + kc * 32 + (cc & 3) * 8);
     }
   };
@@ -450,7 +458,7 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
       const int e = tid + i * NT;
       if (CHUNK16 % NT == 0 || e < CHUNK16) {
         const int r = e / (U * 4), cc = e % (U * 4);
-        const bool ok = r < M && it * U + cc / 4 < KT;
+        const bool ok = r < M && it * U + cc / 4 < KTs;
         *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[p][i] : zero;
       }
     }
@@ -555,6 +563,14 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
       w.x = (uint32_t)f2bf(x[0]) | ((uint32_t)f2bf(x[1]) << 16);
       w.y = (uint32_t)f2bf(x[2]) | ((uint32_t)f2bf(x[3]) << 16);
       *(u32x2*)(dst + dim0) = w;
+    }
+  } else if constexpr (EPI == kEpiPartial) {
+    // lane: features grp * 16 + (lane / 16) * 4 .. + 3 of rows jf * 16 + lane % 16
+    const int n0 = grp * 16 + (lane >> 4) * 4;
+#pragma unroll
+    for (int jf = 0; jf < MF; ++jf) {
+      const int m = jf * 16 + (lane & 15);
+      if (m < M) *(f32x4*)(ep.C + ((long)sp * M + m) * N + n0) = acc[jf];
     }
   } else if constexpr (EPI == kEpiConf) {
     // lane: vocabulary ids v0 .. v0 + 3 of rows jf * 16 + lane % 16
@@ -757,6 +773,40 @@ hipError_t gemm_bf16_swiglu_fused(const uint16_t* X, int ldx, const void* Wp, in
   ep.out = out;
   ep.F = F;
   return launch_fused<kEpiSwiGlu, 4>(X, ldx, Wp, M, 2 * F, K, ep, wsc, st, e0, e1);
+}
+
+hipError_t gemm_bf16_split_fused(const uint16_t* X, int ldx, const void* Wp, float* C, int M,
+                                 int N, int K, int gw, int splits, int ks, hipStream_t st,
+                                 hipEvent_t e0, hipEvent_t e1, const float* wsc) {
+  const int KT = K / 32;
+  if (M < 1 || M > 64 || N % 16 || K % 32 || ks <= 0 || splits <= 0 ||
+      (long)splits * ks < KT || (long)(splits - 1) * ks >= KT || (N / 16) % gw ||
+      (wsc && (K % 64 || ks % 2)))
+    return hipErrorInvalidValue;
+  FusedEpi ep{};
+  ep.C = C;
+  ep.splits = splits;
+  ep.ks = ks;
+  const dim3 grid(N / 16 / gw * splits);
+  const u32x4* W = (const u32x4*)Wp;
+#define WD_SPLIT_GW(GWV)                                                                       \
+  case GWV:                                                                                    \
+    if (wsc)                                                                                   \
+      launch_fused_mf<kEpiPartial, 4, true, GWV, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st,  \
+                                                       e0, e1);                                \
+    else                                                                                       \
+      launch_fused_mf<kEpiPartial, 4, false, GWV, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, \
+                                                        e0, e1);                               \
+    break;
+  switch (gw) {
+    WD_SPLIT_GW(2)
+    WD_SPLIT_GW(3)
+    WD_SPLIT_GW(4)
+    WD_SPLIT_GW(6)
+    default: return hipErrorInvalidValue;
+  }
+#undef WD_SPLIT_GW
+  return hipGetLastError();
 }
 
 // ---- bf16 GEMM for many rows (refresh steps, the full-sequence path, batches) ----------
@@ -1121,6 +1171,21 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
     p.ck = 1;
     return p;
   }
+  if (M <= 64 && !w8 && K >= 2 * N && N % 64 == 0) {
+    // a long K (down): the pipelined kernel with partials, 4 groups per
+    // workgroup and the most power-of-two splits that keep one round of
+    // workgroups, each split at least 16 K steps (measured with weights
+    // read from HBM, 33-39 rows: 4096 x 12288 18.5 us against 19.5 for the
+    // kernel below, 18944 x 3584 25.5 against 26.3)
+    int S = 1;
+    while (2 * S <= max_splits && (long)(N / 64) * 2 * S <= 256 && KT / (2 * S) >= 16) S *= 2;
+    p.fused_gw = 4;
+    p.ks_per_split = (KT + S - 1) / S;
+    p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
+    p.grid = (N / 64) * p.splits;
+    p.mf = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
+    return p;
+  }
   if (M <= 64) {
     p.nf = (N >= 16384 && N % 128 == 0) ? 2 : 1;
     p.mf = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
@@ -1165,6 +1230,11 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
                      const GemmPlan& p, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
                      const float* wsc) {
   if (M <= 0) return hipSuccess;
+  if (p.fused_gw) {
+    if ((long)(N / 16 / p.fused_gw) * p.splits != p.grid) return hipErrorInvalidValue;
+    return gemm_bf16_split_fused(X, ldx, Wp, C, M, N, K, p.fused_gw, p.splits, p.ks_per_split, st,
+                                 ev_start, ev_stop, wsc);
+  }
   if (p.dma_mfw) {
     const int NB = N / 256, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
     const int KT = K / 32;

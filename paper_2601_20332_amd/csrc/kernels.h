@@ -20,6 +20,7 @@ struct GemmPlan {
   int ks_per_split = 0;  // 32-wide K steps per split
   int grid = 0;
   int dma_mfw = 0;       // > 0: k_gemm_bf16_dma with 64 * dma_mfw-row tiles
+  int fused_gw = 0;      // > 0: gemm_bf16_split_fused with fused_gw groups per workgroup
 };
 // Launch plan for C = X W^T; at most max_splits K splits.
 GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8 = false, int max_splits = 1 << 20);
@@ -37,8 +38,14 @@ hipError_t pack_fp8(const uint16_t* W, int N, int K, void* out, float* scale, hi
 // kPackRopePair, head_dim 128; writes q [M][nh][128] and the k/v cache rows
 // row_tok of each head.  SwiGLU: weights packed kPackGateUp (N = 2F);
 // writes out [M][F] = silu(gate) * up.
-constexpr int kEpiQkv = 1, kEpiSwiGlu = 2, kEpiConf = 3;
+constexpr int kEpiQkv = 1, kEpiSwiGlu = 2, kEpiConf = 3, kEpiPartial = 4;
 bool fused_rows_ok(int M, int N, int K);
+// The same pipelined few-row kernel over K splits (1 <= M <= 64): gw 16-row
+// weight groups per workgroup (2, 3, 4 or 6; N / 16 a multiple of it), split
+// s covering K steps [s ks, s ks + ks); writes C[s][m][n] fp32 like gemm_bf16.
+hipError_t gemm_bf16_split_fused(const uint16_t* X, int ldx, const void* Wp, float* C, int M,
+                                 int N, int K, int gw, int splits, int ks, hipStream_t st,
+                                 hipEvent_t e0, hipEvent_t e1, const float* wsc);
 hipError_t gemm_bf16_qkv_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
                                const uint16_t* bias, const float* rope_cs, const int32_t* row_pos,
                                const int32_t* row_tok, int nh, int nkv, uint16_t* q, uint16_t* kc,
