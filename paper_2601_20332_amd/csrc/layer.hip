@@ -253,10 +253,19 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float* __restrict__ q,
 // stay in registers in exactly the layout the second product needs.  Softmax
 // runs online in fp32; P enters the bf16 MFMA as hi + lo bf16 parts, which
 // keeps P V at fp32-level accuracy.
+//
+// Key order inside a tile: key = 16 kq + k16 sits at V^T position 4 k16 + kq,
+// so a thread that loaded keys t, t + 16, t + 32, t + 48 writes each of its
+// dims as one 8-byte store.  Row r of score subtile st is key
+// pi(st, r) = 16 (r % 4) + 8 (st / 2) + 2 (r / 4) + st % 2 (K is stored at that
+// row), which puts in each lane exactly the scores its P operand needs for the
+// V^T positions it multiplies.  V^T rows are 64 keys (8 chunks of 16 bytes);
+// chunk j of dim d is stored at chunk j ^ ((d / 8) % 8), which spreads both
+// the stores and the 16-byte operand reads over the banks.
 constexpr int kAttD = 128;
 constexpr int kKT = 64;              // keys per tile
 constexpr int kKPitch = kAttD + 8;   // bf16 elements per K row in LDS
-constexpr int kVPitch = kKT + 8;     // bf16 elements per V^T row in LDS
+constexpr int kVPitch = kKT;         // bf16 elements per V^T row in LDS (swizzled chunks)
 constexpr int kMaxSplit = 16;        // most key splits of one attention launch
 
 // Split-KV: blockIdx.z = query block * nsplit + split; split s covers keys
@@ -305,9 +314,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
   const float scale = 0.08838834764831845f;  // 1/sqrt(128)
 
   // K/V tile of 64 keys x 256 B each: thread tid covers keys (tid >> 4) + 16 i,
-  // 16-byte chunk tid & 15.  The next tile's loads are issued before the
-  // current tile is computed; addresses are clamped to the last key and the
-  // keys past c are zeroed when the tile is stored.
+  // 16-byte chunk tid & 15 (dims 8 (tid & 15) ..).  The next tile's loads are
+  // issued before the current tile is computed; addresses are clamped to the
+  // last key and the keys past c are zeroed when the tile is stored.
   const int tkey = tid >> 4, tch = tid & 15;
   u32x4 kr[4], vr[4];
   auto load_tile = [&](int j0) {
@@ -321,17 +330,26 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
   if (key_lo < c) load_tile(key_lo);
   for (int j0 = key_lo; j0 < c; j0 += kKT) {
     __syncthreads();
-    // K rows as they are; V transposed into Vt[dd][key]
+    // K rows at the score row that holds them; V^T dims as 4-key runs
+    u32x4 vv[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int key = tkey + 16 * i;
+      const int key = tkey + 16 * i;  // k16 = tkey, kq = i
       const bool ok = j0 + key < c;
-      const u32x4 kv = ok ? kr[i] : zero4, vv = ok ? vr[i] : zero4;
-      *(u32x4*)(Ks + key * kKPitch + tch * 8) = kv;
+      const u32x4 kv = ok ? kr[i] : zero4;
+      vv[i] = ok ? vr[i] : zero4;
+      const int st = 2 * (tkey >> 3) + (tkey & 1), r = 4 * ((tkey >> 1) & 3) + i;
+      *(u32x4*)(Ks + (st * 16 + r) * kKPitch + tch * 8) = kv;
+    }
+    {
+      const int chunk = (tkey >> 1) ^ (tch & 7);  // dims tch * 8 .. have d / 8 = tch
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        Vt[(tch * 8 + 2 * w) * kVPitch + key] = (uint16_t)(vv[w] & 0xffffu);
-        Vt[(tch * 8 + 2 * w + 1) * kVPitch + key] = (uint16_t)(vv[w] >> 16);
+      for (int e = 0; e < 8; ++e) {
+        const int sh = 16 * (e & 1);
+        u32x2 w;
+        w.x = ((vv[0][e >> 1] >> sh) & 0xffffu) | (((vv[1][e >> 1] >> sh) & 0xffffu) << 16);
+        w.y = ((vv[2][e >> 1] >> sh) & 0xffffu) | (((vv[3][e >> 1] >> sh) & 0xffffu) << 16);
+        *(u32x2*)(Vt + (tch * 8 + e) * kVPitch + chunk * 8 + (tkey & 1) * 4) = w;
       }
     }
     __syncthreads();
@@ -349,13 +367,13 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
         sacc[st] = mfma16(ka, qf[cc], sacc[st]);
       }
     }
-    // this lane holds keys st*16 + grp*4 + jj for query l16
+    // this lane holds keys pi(st, grp * 4 + jj) for query l16
     float tmax = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const int key = j0 + st * 16 + grp * 4 + jj;
+        const int key = j0 + 16 * jj + 8 * (st >> 1) + 2 * grp + (st & 1);
         const float s = key < c ? sacc[st][jj] * scale : -INFINITY;
         sacc[st][jj] = s;
         tmax = fmaxf(tmax, s);
@@ -380,10 +398,11 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
 #pragma unroll
     for (int i = 0; i < 8; ++i) oacc[i] *= corr;
 
-    // O^T += V^T P^T over two 32-key chunks (subtiles 2pc, 2pc+1)
+    // O^T += V^T P^T over two 32-position chunks (subtiles 2pc, 2pc+1)
 #pragma unroll
     for (int pc = 0; pc < 2; ++pc) {
-      // element e of the fragment is key index (e < 4 ? subtile 2pc : 2pc+1), row grp*4 + e%4
+      // element e of lane grp's fragment is V^T position 32 pc + 8 grp + e, the key
+      // of score subtile 2 pc + e / 4, row grp * 4 + e % 4
       u32x4 bhi, blo;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -395,10 +414,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
       }
 #pragma unroll
       for (int df = 0; df < 8; ++df) {
-        const uint16_t* vrow = Vt + (df * 16 + l16) * kVPitch;
-        const u32x2 v0 = *(const u32x2*)(vrow + (2 * pc) * 16 + grp * 4);
-        const u32x2 v1 = *(const u32x2*)(vrow + (2 * pc + 1) * 16 + grp * 4);
-        const u32x4 va = {v0.x, v0.y, v1.x, v1.y};
+        const int d = df * 16 + l16;
+        const u32x4 va = *(const u32x4*)(Vt + d * kVPitch + (((4 * pc + grp) ^ ((d >> 3) & 7)) * 8));
         oacc[df] = mfma16(va, bhi, oacc[df]);
         oacc[df] = mfma16(va, blo, oacc[df]);
       }
