@@ -939,6 +939,14 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
       WD_HIP(wd::gemm_bf16_swiglu_fused((const uint16_t*)a, H, w.wgu, M, F, H, (uint16_t*)sw, st,
                                         e0, e1, w.sgu));
       WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, 2 * F, H, m.esz, (double)M * F * m.esz));
+    } else if (const wd::GemmPlan gp = wd::plan_gemm_bf16(M, 2 * F, H);
+               c.dtype == WD_DTYPE_BF16 && !w.sgu && gp.dma_mfw && gp.splits == 1) {
+      // many rows without a K split: SwiGLU in the GEMM's epilogue
+      hipEvent_t e0, e1;
+      WD_TRY(profile_begin(m_mut(s), &e0, &e1));
+      WD_HIP(wd::gemm_bf16_swiglu_dma((const uint16_t*)a, H, w.wgu, (uint16_t*)sw, M, F, H, gp, st,
+                                      e0, e1));
+      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_TILED, M, 2 * F, H, m.esz, (double)M * F * m.esz));
     } else {
       WD_TRY(gemm<T>(s, a, H, w.wgu, w.sgu, s->C, M, 2 * F, H, 1 << 20, &S));
       WD_HIP(wd::swiglu<T>(s->C, S, M, F, sw, st));

@@ -992,11 +992,16 @@ __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
 // every LDS operation of this wave complete (lgkmcnt 0; vmcnt, expcnt free)
 #define WD_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xC07F)
 
-template <int MFW, int ST>
+// SWIGLU (no K split, weights packed kPackGateUp): lane values of packed
+// groups 2 i + h come as gate (e / 4 = 2 h) and up (e / 4 = 2 h + 1) of the
+// same features, so the epilogue writes out[m][f] = silu(gate) * up (bf16,
+// F = N / 2 per row) instead of the fp32 products.
+template <int MFW, int ST, bool SWIGLU = false>
 __global__ __launch_bounds__(256, 1) void k_gemm_bf16_dma(const uint16_t* __restrict__ X, int ldx,
                                                           const u32x4* __restrict__ Wp,
                                                           float* __restrict__ C, int M, int N,
-                                                          int K, int NB, int MT, int S, int ks) {
+                                                          int K, int NB, int MT, int S, int ks,
+                                                          uint16_t* __restrict__ out) {
   // the host pass only needs the kernel's signature
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int NFW = 4;
@@ -1113,6 +1118,25 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16_dma(const uint16_t* __rest
     for (int jj = 0; jj < MFW; ++jj) {
       const int m = m0 + (wm * MFW + jj) * 32 + (lane & 31);
       if (m >= M) continue;
+      if constexpr (SWIGLU) {
+        const int F = N >> 1;
+        const int i = nb * 2 * NFW + wn * NFW + ii;
+#pragma unroll
+        for (int hg = 0; hg < 2; ++hg) {
+          const int f0 = (2 * i + hg) * 8 + (lane >> 5) * 4;
+          float y[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float x = acc[ii][jj][8 * hg + j], u = acc[ii][jj][8 * hg + 4 + j];
+            y[j] = x / (1.0f + expf(-x)) * u;
+          }
+          u32x2 w;
+          w.x = (uint32_t)f2bf(y[0]) | ((uint32_t)f2bf(y[1]) << 16);
+          w.y = (uint32_t)f2bf(y[2]) | ((uint32_t)f2bf(y[3]) << 16);
+          *(u32x2*)(out + (long)m * F + f0) = w;
+        }
+        continue;
+      }
       const int n0 = (nb * 2 * NFW + wn * NFW + ii) * 32 + (lane >> 5) * 4;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -1171,12 +1195,13 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
     p.ck = 1;
     return p;
   }
-  if (M <= 64 && !w8 && K >= 2 * N && N % 64 == 0) {
-    // a long K (down): the pipelined kernel with partials, 4 groups per
-    // workgroup and the most power-of-two splits that keep one round of
-    // workgroups, each split at least 16 K steps (measured with weights
-    // read from HBM, 33-39 rows: 4096 x 12288 18.5 us against 19.5 for the
-    // kernel below, 18944 x 3584 25.5 against 26.3)
+  if (M <= 64 && !w8 && K >= N && N % 64 == 0) {
+    // K at least N (O, down): the pipelined kernel with partials, 4 groups
+    // per workgroup and the most power-of-two splits that keep one round of
+    // workgroups, each split at least 16 K steps (measured with weights read
+    // from HBM, 33-39 rows: 4096 x 12288 18.5 us against 19.5 for the kernel
+    // below, 18944 x 3584 25.5 against 26.3, 4096 x 4096 9.2 against 9.2
+    // with 4 splits instead of 8, which halves what the residual norm reads)
     int S = 1;
     while (2 * S <= max_splits && (long)(N / 64) * 2 * S <= 256 && KT / (2 * S) >= 16) S *= 2;
     p.fused_gw = 4;
@@ -1244,13 +1269,13 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
     const dim3 grid(p.grid);
     if (p.dma_mfw == 4)
       launch_timed(k_gemm_bf16_dma<4, 3>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
-                   M, N, K, NB, MT, p.splits, p.ks_per_split);
+                   M, N, K, NB, MT, p.splits, p.ks_per_split, (uint16_t*)nullptr);
     else if (p.dma_mfw == 3)
       launch_timed(k_gemm_bf16_dma<3, 4>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
-                   M, N, K, NB, MT, p.splits, p.ks_per_split);
+                   M, N, K, NB, MT, p.splits, p.ks_per_split, (uint16_t*)nullptr);
     else if (p.dma_mfw == 2)
       launch_timed(k_gemm_bf16_dma<2, 4>, grid, st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C,
-                   M, N, K, NB, MT, p.splits, p.ks_per_split);
+                   M, N, K, NB, MT, p.splits, p.ks_per_split, (uint16_t*)nullptr);
     else
       return hipErrorInvalidValue;
     return hipGetLastError();
@@ -1276,6 +1301,31 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
   WD_GEMM_CASE(1, 8) WD_GEMM_CASE(2, 8)
 #undef WD_GEMM_CASE
   if (!launched) return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t gemm_bf16_swiglu_dma(const uint16_t* X, int ldx, const void* Wp, uint16_t* out, int M,
+                                int F, int K, const GemmPlan& p, hipStream_t st,
+                                hipEvent_t ev_start, hipEvent_t ev_stop) {
+  const int N = 2 * F;
+  if (M <= 0) return hipSuccess;
+  const int NB = N / 256, KT = K / 32;
+  const int MT = p.dma_mfw ? (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw) : 0;
+  if (!p.dma_mfw || p.splits != 1 || N % 256 || K % 32 || NB * MT != p.grid ||
+      p.ks_per_split < KT)
+    return hipErrorInvalidValue;
+  const dim3 grid(p.grid);
+  if (p.dma_mfw == 4)
+    launch_timed(k_gemm_bf16_dma<4, 3, true>, grid, st, ev_start, ev_stop, X, ldx,
+                 (const u32x4*)Wp, (float*)nullptr, M, N, K, NB, MT, 1, KT, out);
+  else if (p.dma_mfw == 3)
+    launch_timed(k_gemm_bf16_dma<3, 4, true>, grid, st, ev_start, ev_stop, X, ldx,
+                 (const u32x4*)Wp, (float*)nullptr, M, N, K, NB, MT, 1, KT, out);
+  else if (p.dma_mfw == 2)
+    launch_timed(k_gemm_bf16_dma<2, 4, true>, grid, st, ev_start, ev_stop, X, ldx,
+                 (const u32x4*)Wp, (float*)nullptr, M, N, K, NB, MT, 1, KT, out);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

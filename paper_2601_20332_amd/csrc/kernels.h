@@ -40,6 +40,12 @@ hipError_t pack_fp8(const uint16_t* W, int N, int K, void* out, float* scale, hi
 // writes out [M][F] = silu(gate) * up.
 constexpr int kEpiQkv = 1, kEpiSwiGlu = 2, kEpiConf = 3, kEpiPartial = 4;
 bool fused_rows_ok(int M, int N, int K);
+// Many-row gate/up with SwiGLU in the epilogue: p must be a k_gemm_bf16_dma
+// plan without a K split for (M, 2F, K); weights packed kPackGateUp; writes
+// out [M][F] = silu(gate) * up.
+hipError_t gemm_bf16_swiglu_dma(const uint16_t* X, int ldx, const void* Wp, uint16_t* out, int M,
+                                int F, int K, const GemmPlan& p, hipStream_t st,
+                                hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 // The same pipelined few-row kernel over K splits (1 <= M <= 64): gw 16-row
 // weight groups per workgroup (2, 3, 4 or 6; N / 16 a multiple of it), split
 // s covering K steps [s ks, s ks + ks); writes C[s][m][n] fp32 like gemm_bf16.
