@@ -294,12 +294,16 @@ def other_workload(name: str, device: str):
     }
 
 
-def generation(model, prompts, G, wc, n_steps, full=False):
+def generation(model, prompts, G, wc, n_steps, full=False, progress=None):
+    """One whole generation; with progress, a log line every `progress` steps
+    (long full-sequence runs)."""
     import paper_2601_20332_amd as wd
     gen = wd.wd_prefill_prompt(model, prompts, G, wc)
     fn = wd.lib.wd_full_step if full else wd.lib.wd_step
-    for _ in range(n_steps):
+    for i in range(n_steps):
         wd._check(fn(gen.handle, None))
+        if progress and (i + 1) % progress == 0:
+            log(f"[bench] {'full-sequence' if full else 'windowed'} step {i + 1}/{n_steps}")
     gen.free()  # synchronizes the stream
 
 
@@ -465,6 +469,9 @@ def main():
                     choices=["llada8b", "dream7b", "llada8b_long", "llada8b_batch16"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full", action="store_true", help="skip the full-sequence comparison")
+    ap.add_argument("--full-once", action="store_true",
+                    help="time the full-sequence generation without a warm-up run of its own "
+                         "(the kernels are warm from the windowed runs)")
     ap.add_argument("--no-eos", action="store_true",
                     help="skip the adaptive-termination measurement")
     ap.add_argument("--no-variants", action="store_true",
@@ -552,13 +559,18 @@ def main():
         wd.wd_profile_enable(model, False)
         if roofline:
             roofline["instrumented_pass_s"] = round(elapsed_ev, 3)
+        if args.workload != "llada8b":
+            for r in (roofline, roofline_tiled, roofline_attn):
+                if r:
+                    r["traffic"] = None  # the counter runs cover the LLaDA-8B workload
 
     full_speedup = None
     if not args.no_full:
-        generation(model, prompts, w.gen_len, wc, n_steps, full=True)  # warm
+        if not args.full_once:
+            generation(model, prompts, w.gen_len, wc, n_steps, full=True)  # warm
         torch.cuda.synchronize()
         tf = time.perf_counter()
-        generation(model, prompts, w.gen_len, wc, n_steps, full=True)
+        generation(model, prompts, w.gen_len, wc, n_steps, full=True, progress=64)
         torch.cuda.synchronize()
         t_full = time.perf_counter() - tf
         full_speedup = round(t_full / (elapsed / args.steps), 3)
