@@ -155,7 +155,7 @@ def roofline_of(model, kernel_class: int, elapsed_ev: float):
     tfs = alg_flops / launches / avg_s / 1e12
     hbm = kernel_class in (1, 4)
     achieved, peak = (gbs, HBM_PEAK_GBS) if hbm else (tfs, BF16_PEAK_TFLOPS)
-    label = {1: " + k_gemm_bf16_fused (at most 64 rows)", 2: " (more than 64 rows)",
+    label = {1: " + k_gemm_bf16_fused (at most 64 rows; 96 for gate/up, O, down)", 2: " (more rows)",
              4: " + k_attn_combine (one layer's attention)"}[kernel_class]
     return {
         "kernel": name + label,

@@ -282,9 +282,10 @@ wd_status wd_debug_weight_row(const wd_model* m, int32_t tensor, int32_t row, fl
 /* Kernel classes of the recorded GEMM launches. */
 enum {
   WD_PROF_ALL = 0,        /* every recorded launch */
-  WD_PROF_GEMM_ROWS = 1,  /* k_gemm_bf16: at most 64 rows, each weight read once (normal
-                             steps, LM head) */
-  WD_PROF_GEMM_TILED = 2, /* more than 64 rows (refresh and full-sequence steps):
+  WD_PROF_GEMM_ROWS = 1,  /* k_gemm_bf16 / k_gemm_bf16_fused: at most 64 rows (96 for
+                             gate/up, O and down), each weight read once (normal steps,
+                             LM head) */
+  WD_PROF_GEMM_TILED = 2, /* more rows (refresh and full-sequence steps):
                              k_gemm_bf16_dma (bf16, widths a multiple of 256), else
                              k_gemm_bf16_big */
   WD_PROF_GEMM_F32 = 3,   /* k_gemm_f32: fp32 models */

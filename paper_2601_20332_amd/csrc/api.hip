@@ -881,8 +881,8 @@ wd_status gemm(wd_seq* s, const T* X, int ldx, const void* W, const float* wsc, 
 
 // The few-row products that carry their own epilogue (bf16, at most 64 rows,
 // wide enough for one workgroup per 64 features to fill the GPU).
-bool fused_rows(const wd_model& m, int M, int N, int K) {
-  return m.cfg.dtype == WD_DTYPE_BF16 && wd::fused_rows_ok(M, N, K);
+bool fused_rows(const wd_model& m, int M, int N, int K, int epi) {
+  return m.cfg.dtype == WD_DTYPE_BF16 && wd::fused_rows_ok(M, N, K, wd::fused_max_rows(epi));
 }
 
 wd_model& m_mut(wd_seq* s) { return *s->m; }
@@ -905,7 +905,7 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
     const LayerW& w = m.layers[l];
     T* kc = (T*)s->kc + (size_t)l * KVd * s->T;
     T* vc = (T*)s->vc + (size_t)l * KVd * s->T;
-    if (fused_rows(m, M, m.qkv_n, H)) {
+    if (fused_rows(m, M, m.qkv_n, H, wd::kEpiQkv)) {
       hipEvent_t e0, e1;
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_qkv_fused((const uint16_t*)a, H, w.wqkv, M, m.qkv_n, H,
@@ -933,7 +933,7 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
     }
     WD_TRY(gemm<T>(s, o, Q, w.wo, w.so, s->C, M, H, Q, 1 << 20, &S));
     WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)w.ffn_norm, c.rms_eps, a, nullptr, st));
-    if (fused_rows(m, M, 2 * F, H)) {
+    if (fused_rows(m, M, 2 * F, H, wd::kEpiSwiGlu)) {
       hipEvent_t e0, e1;
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_swiglu_fused((const uint16_t*)a, H, w.wgu, M, F, H, (uint16_t*)sw, st,
@@ -990,7 +990,7 @@ wd_status decide(wd_seq* s, int n_act) {
   const wd_model_config& c = m.cfg;
   const int n = s->B * n_act;
   int S;
-  if (fused_rows(m, n, c.vocab, c.hidden)) {
+  if (fused_rows(m, n, c.vocab, c.hidden, wd::kEpiConf)) {
     // the LM head reduces each 64-entry vocabulary tile to the confidence
     // inputs itself; the logits reach memory only when asked for
     const int n_tiles = c.vocab / 64;

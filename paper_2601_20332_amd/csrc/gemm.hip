@@ -659,8 +659,8 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
   }
 }
 
-bool fused_rows_ok(int M, int N, int K) {
-  return M >= 1 && M <= 64 && N % 64 == 0 && K % 32 == 0 && N / 64 >= 192;
+bool fused_rows_ok(int M, int N, int K, int max_rows) {
+  return M >= 1 && M <= max_rows && max_rows <= 96 && N % 64 == 0 && K % 32 == 0 && N / 64 >= 192;
 }
 
 template <int EPI, int U, bool W8, int GW, int R, int XD = 2>
@@ -668,11 +668,21 @@ static void launch_fused_mf(dim3 grid, int M, const uint16_t* X, int ldx, const 
                             int K, const FusedEpi& ep, const float* wsc, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1) {
   const dim3 block(64 * GW);
+  // 65 to 96 rows (gate/up, O and down only): activations two iterations ahead,
+  // which keeps the larger staging within the register file
   switch ((M + 15) / 16) {
     case 1: launch_timed_block(k_gemm_bf16_fused<EPI, 1, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
     case 2: launch_timed_block(k_gemm_bf16_fused<EPI, 2, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
     case 3: launch_timed_block(k_gemm_bf16_fused<EPI, 3, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
-    default: launch_timed_block(k_gemm_bf16_fused<EPI, 4, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 4: launch_timed_block(k_gemm_bf16_fused<EPI, 4, U, W8, GW, R, XD>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc); break;
+    case 5:
+      if constexpr (EPI == kEpiSwiGlu || EPI == kEpiPartial)
+        launch_timed_block(k_gemm_bf16_fused<EPI, 5, U, W8, GW, R, 2>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc);
+      break;
+    default:
+      if constexpr (EPI == kEpiSwiGlu || EPI == kEpiPartial)
+        launch_timed_block(k_gemm_bf16_fused<EPI, 6, U, W8, GW, R, 2>, grid, block, st, e0, e1, X, ldx, W, M, N, K, ep, wsc);
+      break;
   }
 }
 
@@ -722,7 +732,7 @@ template <int EPI, int U>
 static hipError_t launch_fused(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
                                const FusedEpi& ep, const float* wsc, hipStream_t st, hipEvent_t e0,
                                hipEvent_t e1) {
-  if (!fused_rows_ok(M, N, K) || (wsc && K % 64)) return hipErrorInvalidValue;
+  if (!fused_rows_ok(M, N, K, fused_max_rows(EPI)) || (wsc && K % 64)) return hipErrorInvalidValue;
   const u32x4* W = (const u32x4*)Wp;
   const int gw = EPI == kEpiConf ? 4 : fused_groups_per_wg(N / 16);
   if ((N / 16) % gw) return hipErrorInvalidValue;
@@ -779,7 +789,7 @@ hipError_t gemm_bf16_split_fused(const uint16_t* X, int ldx, const void* Wp, flo
                                  int N, int K, int gw, int splits, int ks, hipStream_t st,
                                  hipEvent_t e0, hipEvent_t e1, const float* wsc) {
   const int KT = K / 32;
-  if (M < 1 || M > 64 || N % 16 || K % 32 || ks <= 0 || splits <= 0 ||
+  if (M < 1 || M > 96 || N % 16 || K % 32 || ks <= 0 || splits <= 0 ||
       (long)splits * ks < KT || (long)(splits - 1) * ks >= KT || (N / 16) % gw ||
       (wsc && (K % 64 || ks % 2)))
     return hipErrorInvalidValue;
@@ -1195,20 +1205,22 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
     p.ck = 1;
     return p;
   }
-  if (M <= 64 && !w8 && K >= N && N % 64 == 0) {
+  if (M <= 96 && !w8 && K >= N && N % 64 == 0) {
     // K at least N (O, down): the pipelined kernel with partials, 4 groups
     // per workgroup and the most power-of-two splits that keep one round of
     // workgroups, each split at least 16 K steps (measured with weights read
     // from HBM, 33-39 rows: 4096 x 12288 18.5 us against 19.5 for the kernel
     // below, 18944 x 3584 25.5 against 26.3, 4096 x 4096 9.2 against 9.2
     // with 4 splits instead of 8, which halves what the residual norm reads)
+    // Up to 96 rows: at 66-94 rows (weights from HBM) O takes 11.0-12.4 us and
+    // down 23.1-25.8 against 14.6-15.4 and 30.2-33.8 on 128-row tiles.
     int S = 1;
     while (2 * S <= max_splits && (long)(N / 64) * 2 * S <= 256 && KT / (2 * S) >= 16) S *= 2;
     p.fused_gw = 4;
     p.ks_per_split = (KT + S - 1) / S;
     p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
     p.grid = (N / 64) * p.splits;
-    p.mf = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
+    p.mf = (M + 15) / 16;
     return p;
   }
   if (M <= 64) {

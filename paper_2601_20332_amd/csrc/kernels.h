@@ -34,12 +34,16 @@ hipError_t pack_frags(const uint16_t* W, int N, int K, void* out, hipStream_t st
 hipError_t pack_fp8(const uint16_t* W, int N, int K, void* out, float* scale, hipStream_t st,
                     int perm = kPackPlain, const uint16_t* W2 = nullptr);
 // Few-row products with their epilogue in the kernel (no K split), for
-// M <= 64 rows when N / 64 >= 192 (fused_rows_ok).  Q/K/V: weights packed
+// M <= fused_max_rows rows when N / 64 >= 192 (fused_rows_ok).  Q/K/V: weights packed
 // kPackRopePair, head_dim 128; writes q [M][nh][128] and the k/v cache rows
 // row_tok of each head.  SwiGLU: weights packed kPackGateUp (N = 2F);
 // writes out [M][F] = silu(gate) * up.
 constexpr int kEpiQkv = 1, kEpiSwiGlu = 2, kEpiConf = 3, kEpiPartial = 4;
-bool fused_rows_ok(int M, int N, int K);
+// Most rows of the fused products: 96 for gate/up (at 66-94 rows it beats the
+// 128-row tiles: 38.7-47.0 us against 44.0-47.4), 64 for Q/K/V and the LM head
+// (the 128-row tiles win there above 64 rows: Q/K/V 26-29 us against 29-40).
+constexpr int fused_max_rows(int epi) { return epi == kEpiSwiGlu ? 96 : 64; }
+bool fused_rows_ok(int M, int N, int K, int max_rows = 64);
 // Many-row gate/up with SwiGLU in the epilogue: p must be a k_gemm_bf16_dma
 // plan without a K split for (M, 2F, K); weights packed kPackGateUp; writes
 // out [M][F] = silu(gate) * up.
