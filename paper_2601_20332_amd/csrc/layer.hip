@@ -12,6 +12,19 @@
 
 namespace wd {
 
+// four consecutive outputs of a normalized row: one 8-byte store for bf16
+template <typename T>
+__device__ __forceinline__ void store4(T* dst, float x0, float x1, float x2, float x3) {
+  if constexpr (sizeof(T) == 2) {
+    u32x2 w;
+    w.x = (uint32_t)Elem<T>::from_f(x0) | ((uint32_t)Elem<T>::from_f(x1) << 16);
+    w.y = (uint32_t)Elem<T>::from_f(x2) | ((uint32_t)Elem<T>::from_f(x3) << 16);
+    *(u32x2*)dst = w;
+  } else {
+    *(f32x4*)dst = f32x4{x0, x1, x2, x3};
+  }
+}
+
 // ---- embedding gather + first RMSNorm ------------------------------------------------
 // One block per row, 1024 threads; H must be a multiple of 4 and at most 16384.
 template <typename T>
@@ -44,8 +57,8 @@ __global__ __launch_bounds__(1024) void k_embed_norm(const int32_t* __restrict__
   for (int it = 0; it < 4; ++it) {
     const int i = (threadIdx.x + it * 1024) * 4;
     if (i < H)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) a[r * H + i + q] = Elem<T>::from_f(v[it][q] * inv * g[it][q]);
+      store4(a + r * H + i, v[it][0] * inv * g[it][0], v[it][1] * inv * g[it][1],
+             v[it][2] * inv * g[it][2], v[it][3] * inv * g[it][3]);
   }
 }
 
@@ -92,8 +105,8 @@ __global__ __launch_bounds__(1024) void k_residual_norm(float* __restrict__ h,
   for (int it = 0; it < 4; ++it) {
     const int i = (threadIdx.x + it * 1024) * 4;
     if (i < H)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) a[(long)dst * H + i + q] = Elem<T>::from_f(v[it][q] * inv * g[it][q]);
+      store4(a + (long)dst * H + i, v[it][0] * inv * g[it][0], v[it][1] * inv * g[it][1],
+             v[it][2] * inv * g[it][2], v[it][3] * inv * g[it][3]);
   }
 }
 
@@ -449,14 +462,19 @@ __global__ __launch_bounds__(128) void k_attn_combine(const float* __restrict__ 
                                                       const float* __restrict__ ml, int nsplit,
                                                       int M, int nh, uint16_t* __restrict__ o) {
   const int r = blockIdx.x, h = blockIdx.y, dd = threadIdx.x;
-  // every split's (m, l, O) in flight at once; nsplit <= kMaxSplit
+  // every split's (m, l, O) in flight at once; nsplit <= kMaxSplit, and only
+  // the splits that exist are loaded (nsplit is uniform, so are the branches)
   float ms[kMaxSplit], ls[kMaxSplit], os[kMaxSplit];
 #pragma unroll
   for (int s = 0; s < kMaxSplit; ++s) {
-    const long pr = ((long)min(s, nsplit - 1) * M + r) * nh + h;
-    ms[s] = ml[pr * 2];
-    ls[s] = ml[pr * 2 + 1];
-    os[s] = part[pr * kAttD + dd];
+    ms[s] = -INFINITY;
+    ls[s] = os[s] = 0.f;
+    if (s < nsplit) {
+      const long pr = ((long)s * M + r) * nh + h;
+      ms[s] = ml[pr * 2];
+      ls[s] = ml[pr * 2 + 1];
+      os[s] = part[pr * kAttD + dd];
+    }
   }
   float mx = -INFINITY;
 #pragma unroll
