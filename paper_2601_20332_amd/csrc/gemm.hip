@@ -974,9 +974,10 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
 // software-pipelined, K splits until 256 workgroups run (split-K partials
 // cost rows*N*4 bytes each).
 // ---- bf16 GEMM for many rows: multi-stage LDS pipeline fed by direct-to-LDS loads -------
-// Workgroup tile: 64 * MFW rows x 256 features; wave (wm, wn) computes
-// 32 * MFW rows x 128 features (4 waves) or 64 features (8 waves) on
-// v_mfma_f32_32x32x16_bf16 (weights as the A operand, activations as B).
+// Workgroup tile: 64 * MFW rows x 32 * TNB features (256 or 192); wave
+// (wm, wn) computes 32 * MFW rows x 32 * TNB / (NW / 2) features (256: 128
+// with 4 waves, 64 with 8; 192: 32 with 12) on v_mfma_f32_32x32x16_bf16
+// (weights as the A operand, activations as B).
 // Each 32-wide K step
 // is one stage in LDS, filled by 16-byte direct-to-LDS loads (lane l of a
 // load lands at +16 l) ST - 1 stages ahead of the step being computed; one
@@ -1007,9 +1008,11 @@ __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
 // groups 2 i + h come as gate (e / 4 = 2 h) and up (e / 4 = 2 h + 1) of the
 // same features, so the epilogue writes out[m][f] = silu(gate) * up (bf16,
 // F = N / 2 per row) instead of the fp32 products.
-// NW: waves per workgroup, 4 (each 128 features of the tile) or 8 (each 64
-// features, two waves per SIMD).
-template <int MFW, int ST, bool SWIGLU = false, int NW = 4>
+// TNB: 32-feature blocks per tile (8: 256 features, 6: 192).  NW: waves per
+// workgroup, in two row halves; the NW / 2 waves of a half split the TNB
+// blocks evenly (8 waves and 256 features: two waves per SIMD, 64 features
+// each).
+template <int MFW, int ST, bool SWIGLU = false, int NW = 4, int TNB = 8>
 __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __restrict__ X, int ldx,
                                                           const u32x4* __restrict__ Wp,
                                                           float* __restrict__ C, int M, int N,
@@ -1017,9 +1020,9 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __
                                                           uint16_t* __restrict__ out) {
   // the host pass only needs the kernel's signature
 #if defined(__HIP_DEVICE_COMPILE__)
-  static_assert(NW == 4 || NW == 8, "waves");
-  constexpr int NFW = 16 / NW;           // 32-feature blocks of each wave
-  constexpr int F = 4 * MFW + 16;        // 1 KB blocks per stage
+  static_assert(NW % 2 == 0 && TNB % (NW / 2) == 0, "waves split the feature blocks evenly");
+  constexpr int NFW = TNB / (NW / 2);    // 32-feature blocks of each wave
+  constexpr int F = 4 * MFW + 2 * TNB;   // 1 KB blocks per stage
   constexpr int FW = (F + NW - 1) / NW;  // blocks wave w loads: w, w + NW, ... below F
   constexpr int FWMIN = F / NW;          // blocks every wave loads
   constexpr int STAGE16 = (F + 1) * 64;  // u32x4 per stage buffer, pad included
@@ -1050,7 +1053,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __
       step16[q] = 4;
     } else {
       const int i = (f - 4 * MFW) >> 1, h = f & 1;
-      const int g = 2 * (nb * 8 + i) + ((lane >> 4) & 1);
+      const int g = 2 * (nb * TNB + i) + ((lane >> 4) & 1);
       const int sl = (lane & 15) + 16 * (2 * h + (lane >> 5));
       src[q] = Wp + ((long)g * KT + kt0) * 64 + sl;
       step16[q] = 64;
@@ -1137,7 +1140,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __
       if (m >= M) continue;
       if constexpr (SWIGLU) {
         const int F = N >> 1;
-        const int i = nb * 8 + wn * NFW + ii;
+        const int i = nb * TNB + wn * NFW + ii;
 #pragma unroll
         for (int hg = 0; hg < 2; ++hg) {
           const int f0 = (2 * i + hg) * 8 + (lane >> 5) * 4;
@@ -1154,7 +1157,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __
         }
         continue;
       }
-      const int n0 = (nb * 8 + wn * NFW + ii) * 32 + (lane >> 5) * 4;
+      const int n0 = (nb * TNB + wn * NFW + ii) * 32 + (lane >> 5) * 4;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 v = {acc[ii][jj][g * 4], acc[ii][jj][g * 4 + 1], acc[ii][jj][g * 4 + 2],
@@ -1165,51 +1168,63 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __
 #endif
 }
 
-// Waves of the many-row kernel: 8 (two per SIMD, 64 features each) measured
-// 2-8% faster than 4 on the refresh shapes (224-384 rows, weights from HBM):
-// Q/K/V at 384 rows 51.7 us against 54.8, gate/up 91.9 against 94.1, down 47.0
-// against 50.7.
-constexpr int kDmaWaves = 8;
+// Waves of the many-row kernel: with 256-feature tiles 8 (two per SIMD, 64
+// features each) measured 2-8% faster than 4 on the refresh shapes (224-384
+// rows, weights from HBM): Q/K/V at 384 rows 51.7 us against 54.8, gate/up
+// 91.9 against 94.1, down 47.0 against 50.7.  With 192-feature tiles 12 (three
+// per SIMD, 32 features each) beat 6 by up to 10%.
+constexpr int kDmaWaves = 8, kDmaWaves192 = 12;
 
 GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
   GemmPlan p;
   const int KT = K / 32;
   if (M > 64 && !w8 && N % 256 == 0) {
-    // k_gemm_bf16_dma: 64 * mfw-row x 256-feature tiles, S K splits.  Measured
-    // on the projection shapes (224 to 600 rows): a grid that fits one round of
-    // one workgroup per CU (128 to 256 workgroups) beats more, smaller
-    // workgroups, and partials cost their epilogue a read each.  So: a
+    // k_gemm_bf16_dma: 64 * mfw-row x (32 * tnb)-feature tiles, S K splits.
+    // Measured on the projection shapes (224 to 600 rows): a grid that fits
+    // one round of one workgroup per CU (128 to 256 workgroups) beats more,
+    // smaller workgroups, and partials cost their epilogue a read each.  So: a
     // one-round grid if there is one, else no K split if the tiles alone give
-    // 256 workgroups; then least work per CU (rounds x rows x K steps), at
-    // least 32 K steps per split, taller tiles, fewer splits.
+    // 256 workgroups; then least work per CU (rounds x rows x features x K
+    // steps), at least 32 K steps per split, taller tiles, fewer splits, wider
+    // tiles.  192-feature tiles (N a multiple of 192 too) fill all 256 CUs
+    // where 256-feature ones leave a quarter idle (weights from HBM): Q/K/V
+    // 12288 x 4096 at 66-384 rows 23-48 us against 25-52, at 1024 rows 96
+    // against 114; gate/up 24576 x 4096 at 66-384 rows 41-89 against 43-96.
+    // Beyond two rounds of workgroups they lose (gate/up at 8000 rows: 1610
+    // against 1440 us), so they are not offered there.
     struct Cand {
-      int mfw, splits, ks;
-      long grid, key[5];
+      int mfw, tnb, splits, ks;
+      long grid, key[6];
     };
-    Cand c[12];
+    Cand c[24];
     int n = 0;
     bool one_round = false, unsplit_fills = false;
-    for (int mfw : {4, 3, 2})
-      for (int S = 1; S <= 8 && S <= max_splits; S *= 2) {
-        const int ks = (KT + S - 1) / S;
-        if (S > 1 && ks < 8) break;
-        const int splits = (KT + ks - 1) / ks;
-        const int MT = (M + 64 * mfw - 1) / (64 * mfw);
-        const long grid = (long)(N / 256) * MT * splits;
-        const long rounds = (grid + 255) / 256;
-        const bool single = grid >= 128 && rounds == 1;
-        one_round |= single;
-        unsplit_fills |= splits == 1 && grid >= 256;
-        c[n++] = {mfw, splits, ks, grid,
-                  {single ? 0 : 1, rounds * mfw * ks, ks >= 32 ? 0 : 1, -mfw, splits}};
-      }
+    for (int tnb : {8, 6}) {
+      if (N % (32 * tnb)) continue;
+      for (int mfw : {4, 3, 2})
+        for (int S = 1; S <= 8 && S <= max_splits; S *= 2) {
+          const int ks = (KT + S - 1) / S;
+          if (S > 1 && ks < 8) break;
+          const int splits = (KT + ks - 1) / ks;
+          const int MT = (M + 64 * mfw - 1) / (64 * mfw);
+          const long grid = (long)(N / (32 * tnb)) * MT * splits;
+          const long rounds = (grid + 255) / 256;
+          if (tnb == 6 && rounds > 2) continue;  // many rounds: wider tiles move fewer bytes
+          const bool single = grid >= 128 && rounds == 1;
+          one_round |= single;
+          unsplit_fills |= splits == 1 && grid >= 256;
+          c[n++] = {mfw, tnb, splits, ks, grid,
+                    {single ? 0 : 1, rounds * mfw * tnb * ks, ks >= 32 ? 0 : 1, -mfw, splits, -tnb}};
+        }
+    }
     const Cand* pick = nullptr;
     for (int i = 0; i < n; ++i) {
       if (!one_round && unsplit_fills && c[i].splits != 1) continue;
-      if (!pick || std::lexicographical_compare(c[i].key, c[i].key + 5, pick->key, pick->key + 5))
+      if (!pick || std::lexicographical_compare(c[i].key, c[i].key + 6, pick->key, pick->key + 6))
         pick = &c[i];
     }
     p.dma_mfw = pick->mfw;
+    p.dma_tnb = pick->tnb;
     p.splits = pick->splits;
     p.ks_per_split = pick->ks;
     p.grid = (int)pick->grid;
@@ -1276,6 +1291,31 @@ static void launch_mf(dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, c
   }
 }
 
+// the k_gemm_bf16_dma instance of plan p (tile rows, tile width, waves);
+// false if the plan names none
+template <bool SWIGLU, typename... A>
+static bool launch_dma(const GemmPlan& p, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                       A... args) {
+  const dim3 b8(64 * kDmaWaves), b6(64 * kDmaWaves192);
+  if (p.dma_tnb == 8) {
+    switch (p.dma_mfw) {
+      case 4: launch_timed_block(k_gemm_bf16_dma<4, 3, SWIGLU, kDmaWaves, 8>, grid, b8, st, e0, e1, args...); return true;
+      case 3: launch_timed_block(k_gemm_bf16_dma<3, 4, SWIGLU, kDmaWaves, 8>, grid, b8, st, e0, e1, args...); return true;
+      case 2: launch_timed_block(k_gemm_bf16_dma<2, 4, SWIGLU, kDmaWaves, 8>, grid, b8, st, e0, e1, args...); return true;
+      default: return false;
+    }
+  }
+  if (p.dma_tnb == 6) {
+    switch (p.dma_mfw) {
+      case 4: launch_timed_block(k_gemm_bf16_dma<4, 3, SWIGLU, kDmaWaves192, 6>, grid, b6, st, e0, e1, args...); return true;
+      case 3: launch_timed_block(k_gemm_bf16_dma<3, 4, SWIGLU, kDmaWaves192, 6>, grid, b6, st, e0, e1, args...); return true;
+      case 2: launch_timed_block(k_gemm_bf16_dma<2, 4, SWIGLU, kDmaWaves192, 6>, grid, b6, st, e0, e1, args...); return true;
+      default: return false;
+    }
+  }
+  return false;
+}
+
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
                      const GemmPlan& p, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
                      const float* wsc) {
@@ -1286,25 +1326,15 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
                                  ev_start, ev_stop, wsc);
   }
   if (p.dma_mfw) {
-    const int NB = N / 256, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
+    const int TN = 32 * p.dma_tnb;
+    const int NB = N / TN, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
     const int KT = K / 32;
-    if (wsc || N % 256 || K % 32 || NB * MT * p.splits != p.grid || p.ks_per_split <= 0 ||
+    if (wsc || (p.dma_tnb != 8 && p.dma_tnb != 6) || N % TN || K % 32 ||
+        NB * MT * p.splits != p.grid || p.ks_per_split <= 0 ||
         (long)p.ks_per_split * p.splits < KT || (long)p.ks_per_split * (p.splits - 1) >= KT)
       return hipErrorInvalidValue;
-    const dim3 grid(p.grid);
-    if (p.dma_mfw == 4)
-      launch_timed_block(k_gemm_bf16_dma<4, 3, false, kDmaWaves>, grid, dim3(64 * kDmaWaves), st,
-                         ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C, M, N, K, NB, MT, p.splits,
-                         p.ks_per_split, (uint16_t*)nullptr);
-    else if (p.dma_mfw == 3)
-      launch_timed_block(k_gemm_bf16_dma<3, 4, false, kDmaWaves>, grid, dim3(64 * kDmaWaves), st,
-                         ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C, M, N, K, NB, MT, p.splits,
-                         p.ks_per_split, (uint16_t*)nullptr);
-    else if (p.dma_mfw == 2)
-      launch_timed_block(k_gemm_bf16_dma<2, 4, false, kDmaWaves>, grid, dim3(64 * kDmaWaves), st,
-                         ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C, M, N, K, NB, MT, p.splits,
-                         p.ks_per_split, (uint16_t*)nullptr);
-    else
+    if (!launch_dma<false>(p, dim3(p.grid), st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C, M,
+                           N, K, NB, MT, p.splits, p.ks_per_split, (uint16_t*)nullptr))
       return hipErrorInvalidValue;
     return hipGetLastError();
   }
@@ -1337,25 +1367,14 @@ hipError_t gemm_bf16_swiglu_dma(const uint16_t* X, int ldx, const void* Wp, uint
                                 hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int N = 2 * F;
   if (M <= 0) return hipSuccess;
-  const int NB = N / 256, KT = K / 32;
+  const int TN = 32 * p.dma_tnb, KT = K / 32;
+  const int NB = N / TN;
   const int MT = p.dma_mfw ? (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw) : 0;
-  if (!p.dma_mfw || p.splits != 1 || N % 256 || K % 32 || NB * MT != p.grid ||
-      p.ks_per_split < KT)
+  if (!p.dma_mfw || (p.dma_tnb != 8 && p.dma_tnb != 6) || p.splits != 1 || N % TN || K % 32 ||
+      NB * MT != p.grid || p.ks_per_split < KT)
     return hipErrorInvalidValue;
-  const dim3 grid(p.grid);
-  if (p.dma_mfw == 4)
-    launch_timed_block(k_gemm_bf16_dma<4, 3, true, kDmaWaves>, grid, dim3(64 * kDmaWaves), st,
-                       ev_start, ev_stop, X, ldx, (const u32x4*)Wp, (float*)nullptr, M, N, K, NB, MT,
-                       1, KT, out);
-  else if (p.dma_mfw == 3)
-    launch_timed_block(k_gemm_bf16_dma<3, 4, true, kDmaWaves>, grid, dim3(64 * kDmaWaves), st,
-                       ev_start, ev_stop, X, ldx, (const u32x4*)Wp, (float*)nullptr, M, N, K, NB, MT,
-                       1, KT, out);
-  else if (p.dma_mfw == 2)
-    launch_timed_block(k_gemm_bf16_dma<2, 4, true, kDmaWaves>, grid, dim3(64 * kDmaWaves), st,
-                       ev_start, ev_stop, X, ldx, (const u32x4*)Wp, (float*)nullptr, M, N, K, NB, MT,
-                       1, KT, out);
-  else
+  if (!launch_dma<true>(p, dim3(p.grid), st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp,
+                        (float*)nullptr, M, N, K, NB, MT, 1, KT, out))
     return hipErrorInvalidValue;
   return hipGetLastError();
 }

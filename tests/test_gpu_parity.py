@@ -91,6 +91,19 @@ MICRO_ODD = synth.ModelShape(n_layers=2, hidden=384, n_heads=3, n_kv_heads=3, he
                              rope_theta=10000.0)
 
 
+# widths that are multiples of both 256 and 192 (Q/K/V 2304, gate/up 3072, O
+# and down 768): the planner takes 192-feature tiles with K splits for all
+# four above 96 rows; 90 + 170 prompt rows give ragged 128-row tiles
+MICRO_W768 = synth.ModelShape(n_layers=2, hidden=768, n_heads=6, n_kv_heads=6, head_dim=128,
+                              ffn=1536, vocab=2048, dtype=synth.DTYPE_BF16, rms_eps=1e-5,
+                              rope_theta=10000.0)
+
+
+def test_bf16_many_row_kernels_192_feature_tiles():
+    prompts = synth.prompts(MICRO_W768, [90, 170])
+    _run_and_check(MICRO_W768, prompts, 48, synth.WindowSettings(8, 32, 4, 2))
+
+
 def test_bf16_many_row_kernels_odd_widths():
     prompts = synth.prompts(MICRO_ODD, [65, 100])
     _run_and_check(MICRO_ODD, prompts, 40, synth.WindowSettings(8, 24, 4, 2))
