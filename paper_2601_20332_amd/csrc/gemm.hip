@@ -974,10 +974,10 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
 // software-pipelined, K splits until 256 workgroups run (split-K partials
 // cost rows*N*4 bytes each).
 // ---- bf16 GEMM for many rows: multi-stage LDS pipeline fed by direct-to-LDS loads -------
-// Workgroup tile: 64 * MFW rows x 32 * TNB features (256 or 192); wave
+// Workgroup tile: 64 * MFW rows x 32 * TNB features (256, 192 or 128); wave
 // (wm, wn) computes 32 * MFW rows x 32 * TNB / (NW / 2) features (256: 128
-// with 4 waves, 64 with 8; 192: 32 with 12) on v_mfma_f32_32x32x16_bf16
-// (weights as the A operand, activations as B).
+// with 4 waves, 64 with 8; 192: 32 with 12; 128: 32 with 8) on
+// v_mfma_f32_32x32x16_bf16 (weights as the A operand, activations as B).
 // Each 32-wide K step
 // is one stage in LDS, filled by 16-byte direct-to-LDS loads (lane l of a
 // load lands at +16 l) ST - 1 stages ahead of the step being computed; one
@@ -1008,7 +1008,7 @@ __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
 // groups 2 i + h come as gate (e / 4 = 2 h) and up (e / 4 = 2 h + 1) of the
 // same features, so the epilogue writes out[m][f] = silu(gate) * up (bf16,
 // F = N / 2 per row) instead of the fp32 products.
-// TNB: 32-feature blocks per tile (8: 256 features, 6: 192).  NW: waves per
+// TNB: 32-feature blocks per tile (8: 256 features, 6: 192, 4: 128).  NW: waves per
 // workgroup, in two row halves; the NW / 2 waves of a half split the TNB
 // blocks evenly (8 waves and 256 features: two waves per SIMD, 64 features
 // each).
@@ -1196,11 +1196,18 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
       int mfw, tnb, splits, ks;
       long grid, key[6];
     };
-    Cand c[24];
+    //
+    // 128-feature tiles are offered only when the pick among the wider ones
+    // splits K into steps shorter than 32: they reach the same grid with half
+    // the splits, so half the partials for the residual norm to read.  O
+    // 4096 x 4096 at 224-384 rows: 17.0-22.8 us with 4 splits against
+    // 18.7-23.1 with 8 (down, with 48-step splits, would lose: 38.5-56.2
+    // against 35.2-45.7).
+    Cand c[36];
     int n = 0;
     bool one_round = false, unsplit_fills = false;
-    for (int tnb : {8, 6}) {
-      if (N % (32 * tnb)) continue;
+    auto add = [&](int tnb) {
+      if (N % (32 * tnb)) return;
       for (int mfw : {4, 3, 2})
         for (int S = 1; S <= 8 && S <= max_splits; S *= 2) {
           const int ks = (KT + S - 1) / S;
@@ -1209,19 +1216,28 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
           const int MT = (M + 64 * mfw - 1) / (64 * mfw);
           const long grid = (long)(N / (32 * tnb)) * MT * splits;
           const long rounds = (grid + 255) / 256;
-          if (tnb == 6 && rounds > 2) continue;  // many rounds: wider tiles move fewer bytes
+          if (tnb < 8 && rounds > 2) continue;  // many rounds: wider tiles move fewer bytes
           const bool single = grid >= 128 && rounds == 1;
           one_round |= single;
           unsplit_fills |= splits == 1 && grid >= 256;
           c[n++] = {mfw, tnb, splits, ks, grid,
                     {single ? 0 : 1, rounds * mfw * tnb * ks, ks >= 32 ? 0 : 1, -mfw, splits, -tnb}};
         }
-    }
-    const Cand* pick = nullptr;
-    for (int i = 0; i < n; ++i) {
-      if (!one_round && unsplit_fills && c[i].splits != 1) continue;
-      if (!pick || std::lexicographical_compare(c[i].key, c[i].key + 6, pick->key, pick->key + 6))
-        pick = &c[i];
+    };
+    auto best = [&]() {
+      const Cand* b = nullptr;
+      for (int i = 0; i < n; ++i) {
+        if (!one_round && unsplit_fills && c[i].splits != 1) continue;
+        if (!b || std::lexicographical_compare(c[i].key, c[i].key + 6, b->key, b->key + 6)) b = &c[i];
+      }
+      return b;
+    };
+    add(8);
+    add(6);
+    const Cand* pick = best();
+    if (pick->ks < 32) {
+      add(4);
+      pick = best();
     }
     p.dma_mfw = pick->mfw;
     p.dma_tnb = pick->tnb;
@@ -1313,6 +1329,14 @@ static bool launch_dma(const GemmPlan& p, dim3 grid, hipStream_t st, hipEvent_t 
       default: return false;
     }
   }
+  if (p.dma_tnb == 4) {
+    switch (p.dma_mfw) {
+      case 4: launch_timed_block(k_gemm_bf16_dma<4, 3, SWIGLU, kDmaWaves, 4>, grid, b8, st, e0, e1, args...); return true;
+      case 3: launch_timed_block(k_gemm_bf16_dma<3, 4, SWIGLU, kDmaWaves, 4>, grid, b8, st, e0, e1, args...); return true;
+      case 2: launch_timed_block(k_gemm_bf16_dma<2, 4, SWIGLU, kDmaWaves, 4>, grid, b8, st, e0, e1, args...); return true;
+      default: return false;
+    }
+  }
   return false;
 }
 
@@ -1329,7 +1353,7 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
     const int TN = 32 * p.dma_tnb;
     const int NB = N / TN, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
     const int KT = K / 32;
-    if (wsc || (p.dma_tnb != 8 && p.dma_tnb != 6) || N % TN || K % 32 ||
+    if (wsc || (p.dma_tnb != 8 && p.dma_tnb != 6 && p.dma_tnb != 4) || N % TN || K % 32 ||
         NB * MT * p.splits != p.grid || p.ks_per_split <= 0 ||
         (long)p.ks_per_split * p.splits < KT || (long)p.ks_per_split * (p.splits - 1) >= KT)
       return hipErrorInvalidValue;
@@ -1370,7 +1394,8 @@ hipError_t gemm_bf16_swiglu_dma(const uint16_t* X, int ldx, const void* Wp, uint
   const int TN = 32 * p.dma_tnb, KT = K / 32;
   const int NB = N / TN;
   const int MT = p.dma_mfw ? (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw) : 0;
-  if (!p.dma_mfw || (p.dma_tnb != 8 && p.dma_tnb != 6) || p.splits != 1 || N % TN || K % 32 ||
+  if (!p.dma_mfw || (p.dma_tnb != 8 && p.dma_tnb != 6 && p.dma_tnb != 4) || p.splits != 1 ||
+      N % TN || K % 32 ||
       NB * MT != p.grid || p.ks_per_split < KT)
     return hipErrorInvalidValue;
   if (!launch_dma<true>(p, dim3(p.grid), st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp,

@@ -20,7 +20,7 @@ struct GemmPlan {
   int ks_per_split = 0;  // 32-wide K steps per split
   int grid = 0;
   int dma_mfw = 0;       // > 0: k_gemm_bf16_dma with 64 * dma_mfw-row tiles
-  int dma_tnb = 8;       // its 32-feature blocks per tile: 8 (256 features) or 6 (192)
+  int dma_tnb = 8;       // its 32-feature blocks per tile: 8, 6 or 4 (256, 192, 128 features)
   int fused_gw = 0;      // > 0: gemm_bf16_split_fused with fused_gw groups per workgroup
 };
 // Launch plan for C = X W^T; at most max_splits K splits.
