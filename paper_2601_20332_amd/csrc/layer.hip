@@ -121,8 +121,8 @@ hipError_t residual_norm(float* h, const float* C, int S, int M, int H, const T*
 }
 
 // ---- QKV epilogue: split-K sum, bias, RoPE, q store, K/V cache scatter ------------------
-// Block (r, slot): slot < n_heads is a query head, then n_kv key heads, then
-// n_kv value heads.  Thread i handles the rotation pair (i, i + d/2).
+// Head slots: hs < n_heads is a query head, then n_kv key heads, then n_kv
+// value heads.  RoPE rotates the pair (i, i + d/2) of a head.
 // bf16 weights are packed with RoPE pairs adjacent (kPackRopePair), so the
 // GEMM's columns of dim i and i + 64 of a head are at group i/8, rows i%8
 // and 8 + i%8; fp32 weights are in plain order.
@@ -135,28 +135,43 @@ __device__ __forceinline__ int qkv_col(int head, int i, int d, int partner) {
 }
 
 template <typename T>
-__global__ void k_qkv_epilogue(const float* __restrict__ C, int S, int M, int N,
-                               const T* __restrict__ bias, const float* __restrict__ rope_cs,
-                               const int32_t* __restrict__ row_pos,
-                               const int32_t* __restrict__ row_tok, int nh, int nkv, int d,
-                               T* __restrict__ q, T* __restrict__ kc, T* __restrict__ vc,
-                               long cache_rows) {
-  const int r = blockIdx.x, hs = blockIdx.y, i = threadIdx.x, half = d >> 1;
+__global__ __launch_bounds__(64) void k_qkv_epilogue(const float* __restrict__ C, int S, int M,
+                                                     int N, const T* __restrict__ bias,
+                                                     const float* __restrict__ rope_cs,
+                                                     const int32_t* __restrict__ row_pos,
+                                                     const int32_t* __restrict__ row_tok, int nh,
+                                                     int nkv, int d, T* __restrict__ q,
+                                                     T* __restrict__ kc, T* __restrict__ vc,
+                                                     long cache_rows) {
+  // a thread takes dims i .. i + 3 of one head and their rotation partners
+  // i + d / 2 .. (16-byte partial loads, 8-byte bf16 stores); a 64-thread
+  // block covers 512 / d heads of row r
+  const int tph = d >> 3, half = d >> 1;
+  const int r = blockIdx.x, hs = blockIdx.y * (64 / tph) + threadIdx.x / tph;
+  if (hs >= nh + 2 * nkv) return;
+  const int i = (threadIdx.x % tph) * 4;
   const int col = hs * d + i;  // feature index of dim i (bias, outputs)
-  float x0, x1;
-  split_sum2(C + (long)r * N + qkv_col<T>(hs, i, d, 0), C + (long)r * N + qkv_col<T>(hs, i, d, 1),
-             (long)M * N, S, x0, x1);
+  f32x4 x0, x1;
+  split_sum2((const f32x4*)(C + (long)r * N + qkv_col<T>(hs, i, d, 0)),
+             (const f32x4*)(C + (long)r * N + qkv_col<T>(hs, i, d, 1)), (long)M * N / 4, S, x0, x1);
   if (bias) {
-    x0 += Elem<T>::load(bias + col);
-    x1 += Elem<T>::load(bias + col + half);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x0[j] += Elem<T>::load(bias + col + j);
+      x1[j] += Elem<T>::load(bias + col + half + j);
+    }
   }
   if (hs < nh + nkv) {
-    const float* cs = rope_cs + ((long)row_pos[r] * half + i) * 2;
-    const float c = cs[0], sn = cs[1];
-    const float y0 = x0 * c - x1 * sn;
-    const float y1 = x1 * c + x0 * sn;
-    x0 = y0;
-    x1 = y1;
+    const f32x4* cs = (const f32x4*)(rope_cs + ((long)row_pos[r] * half + i) * 2);
+    const f32x4 a = cs[0], b = cs[1];  // (cos, sin) of dims i, i + 1 and i + 2, i + 3
+    const float c[4] = {a[0], a[2], b[0], b[2]}, sn[4] = {a[1], a[3], b[1], b[3]};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float y0 = x0[j] * c[j] - x1[j] * sn[j];
+      const float y1 = x1[j] * c[j] + x0[j] * sn[j];
+      x0[j] = y0;
+      x1[j] = y1;
+    }
   }
   T* dst;
   if (hs < nh) {
@@ -166,8 +181,8 @@ __global__ void k_qkv_epilogue(const float* __restrict__ C, int S, int M, int N,
   } else {
     dst = vc + ((long)(hs - nh - nkv) * cache_rows + row_tok[r]) * d;
   }
-  dst[i] = Elem<T>::from_f(x0);
-  dst[i + half] = Elem<T>::from_f(x1);
+  store4(dst + i, x0[0], x0[1], x0[2], x0[3]);
+  store4(dst + i + half, x1[0], x1[1], x1[2], x1[3]);
 }
 
 template <typename T>
@@ -175,10 +190,12 @@ hipError_t qkv_epilogue(const float* C, int S, int M, const T* bias, const float
                         const int32_t* row_pos, const int32_t* row_tok, int n_heads, int n_kv,
                         int head_dim, T* q, T* kcache, T* vcache, long cache_rows, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  const int N = (n_heads + 2 * n_kv) * head_dim;
-  hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(M, n_heads + 2 * n_kv), dim3(head_dim / 2), 0, st, C,
-                     S, M, N, bias, rope_cs, row_pos, row_tok, n_heads, n_kv, head_dim, q, kcache,
-                     vcache, cache_rows);
+  if (head_dim != 64 && head_dim != 128) return hipErrorInvalidValue;
+  const int N = (n_heads + 2 * n_kv) * head_dim, per_block = 512 / head_dim;
+  const int hblocks = (n_heads + 2 * n_kv + per_block - 1) / per_block;
+  hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(M, hblocks), dim3(64), 0, st, C, S, M, N, bias,
+                     rope_cs, row_pos, row_tok, n_heads, n_kv, head_dim, q, kcache, vcache,
+                     cache_rows);
   return hipGetLastError();
 }
 
