@@ -338,6 +338,19 @@ int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, 
                 int32_t* is_refresh, int32_t* ctx_len, int32_t* n_active, int32_t* n_rows,
                 int32_t* n_decode);
 
+/* Tests only.  The launch plan the bf16 projection GEMM takes for an
+ * M x K by K x N product (fp8: fp8 weights; at most max_splits K splits),
+ * as eight integers in out: the kernel (1 pipelined few-row kernel with
+ * K-split partials, 2 many-row LDS-pipelined kernel, 3 split-K tiled kernel),
+ * rows and features of a workgroup tile, K splits, 32-wide K steps per split,
+ * workgroups, waves per workgroup, and whether the launchers accept the plan
+ * (bit 0 as a plain GEMM, bit 1 with the many-row kernel's SwiGLU epilogue).
+ * The step loop plans every projection this way with no split cap.
+ * WD_ERR_INVALID_ARG for sizes below 1, K not a multiple of 32 or NULL out.
+ * Needs no GPU. */
+wd_status wd_debug_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t fp8, int32_t max_splits,
+                             int32_t* out);
+
 /* Message of the last non-OK status on this thread ("" if none). */
 const char* wd_last_error(void);
 

@@ -30,7 +30,8 @@ EXPORTED = ["wd_weight_count", "wd_weight_shape", "wd_model_bytes", "wd_init_mod
             "wd_free_model", "wd_seq_bytes", "wd_prefill_prompt", "wd_slide_window",
             "wd_refresh_buffer", "wd_step", "wd_full_step", "wd_get_state", "wd_debug_logits",
             "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error", "wd_profile_enable",
-            "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row", "wd_debug_keep_logits", "wd_measure_peaks"]
+            "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row", "wd_debug_keep_logits", "wd_measure_peaks",
+            "wd_debug_gemm_plan"]
 
 
 class WdError(RuntimeError):
@@ -104,6 +105,7 @@ def _load() -> ctypes.CDLL:
                               ctypes.POINTER(ctypes.c_float), i32, pi32]),
         "wd_free_seq": (None, [P]),
         "wd_plan": (i32, [i32, i32, ctypes.POINTER(WindowConfig), i32, pi32, pi32, pi32, pi32, pi32]),
+        "wd_debug_gemm_plan": (i32, [i32, i32, i32, i32, i32, pi32]),
         "wd_last_error": (ctypes.c_char_p, []),
         "wd_profile_enable": (i32, [P, i32]),
         "wd_measure_peaks": (i32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
@@ -357,6 +359,18 @@ def wd_plan(n_prompt: int, gen_len: int, win: WindowConfig):
                                                             ("is_refresh", "ctx_len", "n_active",
                                                              "n_rows", "n_decode")])
     return arrs
+
+
+GEMM_PLAN_FIELDS = ("kernel", "rows", "features", "splits", "k_steps_per_split", "workgroups",
+                    "waves", "accepted")
+
+
+def wd_debug_gemm_plan(M: int, N: int, K: int, fp8: bool = False, max_splits: int = 1 << 20):
+    """The bf16 projection GEMM's launch plan for (M, N, K) (host only)."""
+    out = np.zeros(8, np.int32)
+    _check(lib.wd_debug_gemm_plan(int(M), int(N), int(K), int(bool(fp8)), int(max_splits),
+                                  _i32p(out)))
+    return dict(zip(GEMM_PLAN_FIELDS, (int(v) for v in out)))
 
 
 def wd_profile_enable(model: Model, enable: bool = True) -> None:

@@ -1552,4 +1552,24 @@ int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, 
   return t;
 }
 
+wd_status wd_debug_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t fp8, int32_t max_splits,
+                             int32_t* out) {
+  if (!out) return fail(WD_ERR_INVALID_ARG, "NULL argument");
+  if (M < 1 || N < 1 || K < 1 || K % 32 || max_splits < 1)
+    return fail(WD_ERR_INVALID_ARG, "sizes must be positive, K a multiple of 32");
+  const wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K, fp8 != 0, max_splits);
+  int kernel, rows, features, waves;
+  wd::gemm_plan_tile(p, &kernel, &rows, &features, &waves);
+  out[0] = kernel;
+  out[1] = rows;
+  out[2] = features;
+  out[3] = p.splits;
+  out[4] = p.ks_per_split;
+  out[5] = p.grid;
+  out[6] = waves;
+  out[7] = (wd::gemm_plan_ok(p, M, N, K, fp8 != 0, false) ? 1 : 0) |
+           (wd::gemm_plan_ok(p, M, N, K, fp8 != 0, true) ? 2 : 0);
+  return WD_OK;
+}
+
 }  // extern "C"

@@ -1340,23 +1340,65 @@ static bool launch_dma(const GemmPlan& p, dim3 grid, hipStream_t st, hipEvent_t 
   return false;
 }
 
+bool gemm_plan_ok(const GemmPlan& p, int M, int N, int K, bool w8, bool swiglu) {
+  if (M <= 0 || N <= 0 || K <= 0 || K % 32) return false;
+  const int KT = K / 32;
+  if (p.splits < 1 || p.ks_per_split < 1 || (long)p.ks_per_split * p.splits < KT ||
+      (long)p.ks_per_split * (p.splits - 1) >= KT)
+    return false;
+  const bool fp8_steps = K % 64 == 0 && p.ks_per_split % 2 == 0;  // fp8 fragments pair K steps
+  if (p.fused_gw) {
+    const int gw = p.fused_gw;
+    return !swiglu && M <= 96 && N % 16 == 0 && (gw == 2 || gw == 3 || gw == 4 || gw == 6) &&
+           (N / 16) % gw == 0 && (long)(N / 16 / gw) * p.splits == p.grid && (!w8 || fp8_steps);
+  }
+  if (p.dma_mfw) {
+    const int TN = 32 * p.dma_tnb;
+    if (w8 || p.dma_mfw < 2 || p.dma_mfw > 4 ||
+        (p.dma_tnb != 8 && p.dma_tnb != 6 && p.dma_tnb != 4) || N % TN)
+      return false;
+    const long MT = (M + 64L * p.dma_mfw - 1) / (64L * p.dma_mfw);
+    return (long)(N / TN) * MT * p.splits == p.grid && (!swiglu || p.splits == 1);
+  }
+  if (swiglu || (p.nf != 1 && p.nf != 2) ||
+      (p.mf != 1 && p.mf != 2 && p.mf != 3 && p.mf != 4 && p.mf != 8) ||
+      N % (16 * kWaves * p.nf))
+    return false;
+  const long NB = N / (16 * kWaves * p.nf), MT = (M + 16L * p.mf - 1) / (16L * p.mf);
+  return NB * MT * p.splits == p.grid && (!w8 || fp8_steps);
+}
+
+void gemm_plan_tile(const GemmPlan& p, int* kernel, int* rows, int* features, int* waves) {
+  if (p.fused_gw) {
+    *kernel = 1;
+    *rows = 16 * p.mf;
+    *features = 16 * p.fused_gw;
+    *waves = p.fused_gw;
+  } else if (p.dma_mfw) {
+    *kernel = 2;
+    *rows = 64 * p.dma_mfw;
+    *features = 32 * p.dma_tnb;
+    *waves = p.dma_tnb == 6 ? kDmaWaves192 : kDmaWaves;
+  } else {
+    *kernel = 3;
+    *rows = 16 * p.mf;
+    *features = 16 * kWaves * p.nf;
+    *waves = kWaves;
+  }
+}
+
 hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M, int N, int K,
                      const GemmPlan& p, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
                      const float* wsc) {
   if (M <= 0) return hipSuccess;
+  if (!gemm_plan_ok(p, M, N, K, wsc != nullptr, false)) return hipErrorInvalidValue;
   if (p.fused_gw) {
-    if ((long)(N / 16 / p.fused_gw) * p.splits != p.grid) return hipErrorInvalidValue;
     return gemm_bf16_split_fused(X, ldx, Wp, C, M, N, K, p.fused_gw, p.splits, p.ks_per_split, st,
                                  ev_start, ev_stop, wsc);
   }
   if (p.dma_mfw) {
     const int TN = 32 * p.dma_tnb;
     const int NB = N / TN, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
-    const int KT = K / 32;
-    if (wsc || (p.dma_tnb != 8 && p.dma_tnb != 6 && p.dma_tnb != 4) || N % TN || K % 32 ||
-        NB * MT * p.splits != p.grid || p.ks_per_split <= 0 ||
-        (long)p.ks_per_split * p.splits < KT || (long)p.ks_per_split * (p.splits - 1) >= KT)
-      return hipErrorInvalidValue;
     if (!launch_dma<false>(p, dim3(p.grid), st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C, M,
                            N, K, NB, MT, p.splits, p.ks_per_split, (uint16_t*)nullptr))
       return hipErrorInvalidValue;
@@ -1364,8 +1406,6 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
   }
   const int NB = N / (16 * kWaves * p.nf);
   const int MT = (M + 16 * p.mf - 1) / (16 * p.mf);
-  if (NB * MT * p.splits != p.grid || N % (16 * kWaves * p.nf) || K % 32) return hipErrorInvalidValue;
-  if (wsc && (K % 64 || p.ks_per_split % 2)) return hipErrorInvalidValue;
   const dim3 grid(p.grid);
   bool launched = false;
 #define WD_GEMM_CASE(NF, MF)                                                                  \
@@ -1391,13 +1431,9 @@ hipError_t gemm_bf16_swiglu_dma(const uint16_t* X, int ldx, const void* Wp, uint
                                 hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int N = 2 * F;
   if (M <= 0) return hipSuccess;
-  const int TN = 32 * p.dma_tnb, KT = K / 32;
-  const int NB = N / TN;
-  const int MT = p.dma_mfw ? (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw) : 0;
-  if (!p.dma_mfw || (p.dma_tnb != 8 && p.dma_tnb != 6 && p.dma_tnb != 4) || p.splits != 1 ||
-      N % TN || K % 32 ||
-      NB * MT != p.grid || p.ks_per_split < KT)
-    return hipErrorInvalidValue;
+  if (!p.dma_mfw || !gemm_plan_ok(p, M, N, K, false, true)) return hipErrorInvalidValue;
+  const int KT = K / 32, NB = N / (32 * p.dma_tnb);
+  const int MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
   if (!launch_dma<true>(p, dim3(p.grid), st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp,
                         (float*)nullptr, M, N, K, NB, MT, 1, KT, out))
     return hipErrorInvalidValue;

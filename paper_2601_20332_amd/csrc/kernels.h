@@ -25,6 +25,15 @@ struct GemmPlan {
 };
 // Launch plan for C = X W^T; at most max_splits K splits.
 GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8 = false, int max_splits = 1 << 20);
+// Whether plan p can run C = X W^T (M x K by K x N; w8: fp8 weights; swiglu:
+// the many-row kernel's SwiGLU epilogue, which needs all of K in one
+// workgroup).  gemm_bf16 and gemm_bf16_swiglu_dma reject plans for which
+// this is false.
+bool gemm_plan_ok(const GemmPlan& p, int M, int N, int K, bool w8, bool swiglu);
+// The kernel plan p launches (1 pipelined few-row kernel with K-split
+// partials, 2 the many-row LDS-pipelined kernel, 3 the split-K tiled kernel)
+// and its workgroup tile and waves.
+void gemm_plan_tile(const GemmPlan& p, int* kernel, int* rows, int* features, int* waves);
 // Row orders of packed weights (gemm.hip): plain; RoPE pairs adjacent within
 // each 128-row head (Q/K/V); gate and up interleaved by 8 rows (W2 = up).
 constexpr int kPackPlain = 0, kPackRopePair = 1, kPackGateUp = 2;
