@@ -404,18 +404,18 @@ def buffer_refresh_variant(model, prompts, w, n_steps, fixed_s):
     }
 
 
-def cpu_baseline(w, plan):
+def cpu_baseline(w, plan, L_s=4, reps=5):
     """The float64 oracle on a bounded sample of the workload: one refresh forward
-    (the largest retained prefix of the generation) and one normal-step forward
-    (the average online row count), both over 2 of the layers, plus the LM head
-    and confidence on the active rows.  Scaled to the full depth and summed over
-    the generation's schedule (cost per layer taken as linear in the rows)."""
+    (the largest retained prefix of the generation) over L_s of the layers, and
+    the mean of `reps` normal-step forwards (the average online row count) over
+    the same layers and of `reps` LM head + confidence passes on the active rows.
+    Scaled to the full depth and summed over the generation's schedule (cost per
+    layer taken as linear in the rows)."""
     import numpy as np
     from threadpoolctl import threadpool_info
     import synth
     from oracle.model import OracleModel
     from oracle.sampler import confidence
-    L_s = 2
     shape = synth.with_layers(w.model, L_s)
     om = OracleModel(synth.Weights(shape), cache_budget_bytes=64e9)
     for name, _, _ in synth.tensor_specs(shape):
@@ -437,13 +437,15 @@ def cpu_baseline(w, plan):
         cache.V[l][:c_ref] = V[l]
     rows = list(range(w.prompt_len, w.prompt_len + m_norm))
     t2 = time.perf_counter()
-    om.forward_rows(x[rows], rows, cache, c_ref)
+    for _ in range(reps):
+        om.forward_rows(x[rows], rows, cache, c_ref)
     t3 = time.perf_counter()
-    confidence(om.logits(h[:n_act]), shape.mask_id)
+    for _ in range(reps):
+        confidence(om.logits(h[:n_act]), shape.mask_id)
     t4 = time.perf_counter()
     per_row_ref = (t1 - t0) / L_s / c_ref
-    per_row_norm = (t3 - t2) / L_s / m_norm
-    head = t4 - t3
+    per_row_norm = (t3 - t2) / reps / L_s / m_norm
+    head = (t4 - t3) / reps
     L = w.model.n_layers
     total = sum(L * (per_row_ref * p.n_online if p.refresh else per_row_norm * p.n_online) + head
                 for p in plan)
@@ -454,9 +456,10 @@ def cpu_baseline(w, plan):
         "cores": int(threads),
         "kind": "oracle",
         "sample": (f"float64 oracle, {L_s} of {L} layers: refresh forward over {c_ref} rows "
-                   f"({t1 - t0:.1f} s), normal-step forward over {m_norm} rows ({t3 - t2:.1f} s), "
-                   f"LM head + confidence on {n_act} rows ({head:.1f} s); scaled to {L} layers "
-                   f"and the {len(plan)}-step schedule (extrapolated)"),
+                   f"({t1 - t0:.1f} s), normal-step forward over {m_norm} rows "
+                   f"({(t3 - t2) / reps:.3f} s, mean of {reps}), LM head + confidence on {n_act} "
+                   f"rows ({head:.3f} s, mean of {reps}); {t4 - t0:.1f} s in all; scaled to {L} "
+                   f"layers and the {len(plan)}-step schedule (extrapolated)"),
     }
 
 
