@@ -346,7 +346,8 @@ int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, 
  * workgroups, waves per workgroup, and whether the launchers accept the plan
  * (bit 0 as a plain GEMM, bit 1 with the many-row kernel's SwiGLU epilogue).
  * The step loop plans every projection this way with no split cap.
- * WD_ERR_INVALID_ARG for sizes below 1, K not a multiple of 32 or NULL out.
+ * WD_ERR_INVALID_ARG for sizes outside [1, 2^24], K not a multiple of 32 or
+ * NULL out.
  * Needs no GPU. */
 wd_status wd_debug_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t fp8, int32_t max_splits,
                              int32_t* out);

@@ -1555,8 +1555,9 @@ int32_t wd_plan(int32_t n_prompt, int32_t gen_len, const wd_window_config* win, 
 wd_status wd_debug_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t fp8, int32_t max_splits,
                              int32_t* out) {
   if (!out) return fail(WD_ERR_INVALID_ARG, "NULL argument");
-  if (M < 1 || N < 1 || K < 1 || K % 32 || max_splits < 1)
-    return fail(WD_ERR_INVALID_ARG, "sizes must be positive, K a multiple of 32");
+  if (M < 1 || N < 1 || K < 1 || K % 32 || max_splits < 1 || M > (1 << 24) || N > (1 << 24) ||
+      K > (1 << 24))
+    return fail(WD_ERR_INVALID_ARG, "sizes must be in [1, 2^24], K a multiple of 32");
   const wd::GemmPlan p = wd::plan_gemm_bf16(M, N, K, fp8 != 0, max_splits);
   int kernel, rows, features, waves;
   wd::gemm_plan_tile(p, &kernel, &rows, &features, &waves);

@@ -94,3 +94,5 @@ def test_invalid_arguments():
         wd.wd_debug_gemm_plan(0, 256, 256)
     with pytest.raises(wd.WdError):
         wd.wd_debug_gemm_plan(16, 256, 48)
+    with pytest.raises(wd.WdError):
+        wd.wd_debug_gemm_plan(1 << 25, 256, 256)
