@@ -422,11 +422,17 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
   const int kt_begin = EPI == kEpiPartial ? sp * ep.ks : 0;
   const int KTs = EPI == kEpiPartial ? min(KT, kt_begin + ep.ks) - kt_begin : KT;  // this split's
   const int grp = nb * GW + wave;  // this wave's 16-row weight group
+  // without a K split the last workgroup may hold fewer than GW groups: its
+  // spare waves stream the last group again (every wave takes part in the
+  // loop's barriers) and store nothing
+  const int ngroups = N >> 4;
+  const bool live = grp < ngroups;
+  const int grp_ld = min(grp, ngroups - 1);
   // W8: the ring holds raw fp8 fragments (one per two K steps), decoded when used
   constexpr int UW = W8 ? U / 2 : U;
   const int frags = W8 ? KTs / 2 : KTs;
   const u32x4* wp =
-      Wp + ((long)grp * (W8 ? KT / 2 : KT) + (W8 ? kt_begin / 2 : kt_begin)) * 64 + lane;
+      Wp + ((long)grp_ld * (W8 ? KT / 2 : KT) + (W8 ? kt_begin / 2 : kt_begin)) * 64 + lane;
   f32x4 acc[MF];
 #pragma unroll
   for (int b = 0; b < MF; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -501,7 +507,7 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
   [[maybe_unused]] f32x4 qkv_cs[MF][2];
   [[maybe_unused]] int qkv_tok[MF];
   if constexpr (EPI == kEpiQkv) {
-    const int head = grp >> 3, i0 = (grp & 7) * 8 + ((lane >> 4) & 1) * 4;
+    const int head = grp_ld >> 3, i0 = (grp_ld & 7) * 8 + ((lane >> 4) & 1) * 4;
     const int dim0 = (lane >> 5) * 64 + i0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) qkv_bias[j] = ep.bias ? bf2f(ep.bias[head * 128 + dim0 + j]) : 0.f;
@@ -521,6 +527,9 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
   for (int it = 0; it < n_it; it += R)
     static_for<0, R>([&](auto J) { body(J, it + decltype(J)::value); });
 
+  // the confidence epilogue has barriers; its launches divide the groups evenly
+  if constexpr (EPI != kEpiConf)
+    if (!live) return;
   // lane l holds packed rows grp*16 + (l/16)*4 + j (j < 4) of activation rows
   // j*16 + l%16; packed rows 0..7 of a group pair with rows 8..15 (lane l ^ 32)
   const int hi = lane >> 5;               // 0: rows 0..7 of the group, 1: rows 8..15
@@ -687,22 +696,22 @@ static void launch_fused_mf(dim3 grid, int M, const uint16_t* X, int ldx, const 
 }
 
 // GW weight groups (16 features each) per workgroup, one wave each.  A wave
-// streams at a bounded rate (its loop is latency-bound with one wave per
-// SIMD), so a launch is fastest when its workgroups fill the 256 CUs in as
-// few rounds as possible: the least rounds x GW, ties to more groups per
-// workgroup (every workgroup stages all activation rows).  Two groups only
-// when that is still one round.  Measured (33-39 rows): Q/K/V 4096 x 12288
-// 20.1 us with GW 3 against 21.2 with GW 4; 3584 x 4608 15.5 with GW 2
-// against 17.1; gate/up 4096 x 24576 33.7 with GW 6 against 38.9 with GW 4.
-// The LM head's confidence epilogue needs GW 4.
+// streams at a bounded rate (its loop is latency-bound), so a launch is
+// fastest when its workgroups fill the 256 CUs in as few rounds as possible:
+// the least rounds x GW, ties to more groups per workgroup (every workgroup
+// stages all activation rows).  Two groups only when that is still one
+// round.  GW need not divide the groups: the last workgroup's spare waves
+// store nothing.  Measured (33-39 rows): Q/K/V 4096 x 12288 20.1 us with GW 3
+// against 21.2 with GW 4; 3584 x 4608 15.5 with GW 2 against 17.1; gate/up
+// 4096 x 24576 33.7 with GW 6 against 38.9 with GW 4.  The LM head's
+// confidence epilogue needs GW 4.
 static int fused_groups_per_wg(int groups) {
   int best = 4;
   long best_key = LONG_MAX;
-  for (int gw : {6, 4, 3, 2}) {
-    if (groups % gw) continue;
-    const long wgs = groups / gw, rounds = (wgs + 255) / 256;
+  for (int gw : {10, 8, 6, 4, 3, 2}) {
+    const long wgs = (groups + gw - 1) / gw, rounds = (wgs + 255) / 256;
     if (gw == 2 && rounds > 1) continue;
-    const long key = rounds * gw * 8 + (8 - gw);
+    const long key = rounds * gw * 16 + (16 - gw);
     if (key < best_key) {
       best_key = key;
       best = gw;
@@ -715,11 +724,13 @@ template <int EPI, int U, bool W8>
 static void launch_fused_gw(int gw, const uint16_t* X, int ldx, const u32x4* W, int M, int N,
                             int K, const FusedEpi& ep, const float* wsc, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1) {
-  const dim3 grid(N / 16 / gw);
+  const dim3 grid((N / 16 + gw - 1) / gw);
   if constexpr (EPI == kEpiConf) {
     launch_fused_mf<EPI, U, W8, 4, 4, 2>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1);
   } else {
     switch (gw) {
+      case 10: launch_fused_mf<EPI, U, W8, 10, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
+      case 8: launch_fused_mf<EPI, U, W8, 8, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
       case 6: launch_fused_mf<EPI, U, W8, 6, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
       case 3: launch_fused_mf<EPI, U, W8, 3, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
       case 2: launch_fused_mf<EPI, U, W8, 2, 4, 4>(grid, M, X, ldx, W, N, K, ep, wsc, st, e0, e1); break;
@@ -735,7 +746,7 @@ static hipError_t launch_fused(const uint16_t* X, int ldx, const void* Wp, int M
   if (!fused_rows_ok(M, N, K, fused_max_rows(EPI)) || (wsc && K % 64)) return hipErrorInvalidValue;
   const u32x4* W = (const u32x4*)Wp;
   const int gw = EPI == kEpiConf ? 4 : fused_groups_per_wg(N / 16);
-  if ((N / 16) % gw) return hipErrorInvalidValue;
+  if (EPI == kEpiConf && (N / 16) % gw) return hipErrorInvalidValue;
   if (wsc)
     launch_fused_gw<EPI, U, true>(gw, X, ldx, W, M, N, K, ep, wsc, st, e0, e1);
   else
