@@ -824,6 +824,7 @@ hipError_t gemm_bf16_split_fused(const uint16_t* X, int ldx, const void* Wp, flo
     WD_SPLIT_GW(3)
     WD_SPLIT_GW(4)
     WD_SPLIT_GW(6)
+    WD_SPLIT_GW(7)
     default: return hipErrorInvalidValue;
   }
 #undef WD_SPLIT_GW
@@ -1189,6 +1190,39 @@ constexpr int kDmaWaves = 8, kDmaWaves192 = 12;
 GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
   GemmPlan p;
   const int KT = K / 32;
+  if (M <= 96 && !w8 && K >= N && N % 64 == 0) {
+    // K at least N (O, down): the pipelined kernel with partials, 4 groups
+    // per workgroup and the most power-of-two splits that keep one round of
+    // workgroups, each split at least 16 K steps (measured with weights read
+    // from HBM, 33-39 rows: 4096 x 12288 18.5 us against 19.5 for the kernel
+    // below, 18944 x 3584 25.5 against 26.3, 4096 x 4096 9.2 against 9.2
+    // with 4 splits instead of 8, which halves what the residual norm reads)
+    // Up to 96 rows: at 66-94 rows (weights from HBM) O takes 11.0-12.4 us and
+    // down 23.1-25.8 against 14.6-15.4 and 30.2-33.8 on 128-row tiles.
+    // Where 4 groups per workgroup cannot fill the CUs (Dream-7B's 3584-wide
+    // O and down: 224 workgroups), 7 groups with twice the splits may: the
+    // fullest one-round grid wins, ties to fewer splits.
+    const int groups = N / 16;
+    int best_gw = 4, best_S = 1;
+    long best_grid = -1;
+    for (int gw : {4, 7}) {
+      if (groups % gw) continue;
+      int S = 1;
+      while (2 * S <= max_splits && (long)(groups / gw) * 2 * S <= 256 && KT / (2 * S) >= 16) S *= 2;
+      const long grid = (long)(groups / gw) * S;
+      if (grid > best_grid || (grid == best_grid && S < best_S)) {
+        best_grid = grid;
+        best_gw = gw;
+        best_S = S;
+      }
+    }
+    p.fused_gw = best_gw;
+    p.ks_per_split = (KT + best_S - 1) / best_S;
+    p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
+    p.grid = groups / best_gw * p.splits;
+    p.mf = (M + 15) / 16;
+    return p;
+  }
   if (M > 64 && !w8 && N % 256 == 0) {
     // k_gemm_bf16_dma: 64 * mfw-row x (32 * tnb)-feature tiles, S K splits.
     // Measured on the projection shapes (224 to 600 rows): a grid that fits
@@ -1258,24 +1292,6 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
     p.mf = 8;
     p.nf = 4;
     p.ck = 1;
-    return p;
-  }
-  if (M <= 96 && !w8 && K >= N && N % 64 == 0) {
-    // K at least N (O, down): the pipelined kernel with partials, 4 groups
-    // per workgroup and the most power-of-two splits that keep one round of
-    // workgroups, each split at least 16 K steps (measured with weights read
-    // from HBM, 33-39 rows: 4096 x 12288 18.5 us against 19.5 for the kernel
-    // below, 18944 x 3584 25.5 against 26.3, 4096 x 4096 9.2 against 9.2
-    // with 4 splits instead of 8, which halves what the residual norm reads)
-    // Up to 96 rows: at 66-94 rows (weights from HBM) O takes 11.0-12.4 us and
-    // down 23.1-25.8 against 14.6-15.4 and 30.2-33.8 on 128-row tiles.
-    int S = 1;
-    while (2 * S <= max_splits && (long)(N / 64) * 2 * S <= 256 && KT / (2 * S) >= 16) S *= 2;
-    p.fused_gw = 4;
-    p.ks_per_split = (KT + S - 1) / S;
-    p.splits = (KT + p.ks_per_split - 1) / p.ks_per_split;
-    p.grid = (N / 64) * p.splits;
-    p.mf = (M + 15) / 16;
     return p;
   }
   if (M <= 64) {
@@ -1360,7 +1376,7 @@ bool gemm_plan_ok(const GemmPlan& p, int M, int N, int K, bool w8, bool swiglu) 
   const bool fp8_steps = K % 64 == 0 && p.ks_per_split % 2 == 0;  // fp8 fragments pair K steps
   if (p.fused_gw) {
     const int gw = p.fused_gw;
-    return !swiglu && M <= 96 && N % 16 == 0 && (gw == 2 || gw == 3 || gw == 4 || gw == 6) &&
+    return !swiglu && M <= 96 && N % 16 == 0 && (gw == 2 || gw == 3 || gw == 4 || gw == 6 || gw == 7) &&
            (N / 16) % gw == 0 && (long)(N / 16 / gw) * p.splits == p.grid && (!w8 || fp8_steps);
   }
   if (p.dma_mfw) {

@@ -38,7 +38,7 @@ def _check(M, N, K, fp8, max_splits=1 << 20):
     tiles = -(-M // p["rows"]) * (N // p["features"])
     assert p["workgroups"] == tiles * p["splits"], where
     if p["kernel"] == 1:  # pipelined few-row kernel: every row in one tile
-        assert M <= 96 and p["rows"] >= M and p["waves"] in (2, 3, 4, 6), where
+        assert M <= 96 and p["rows"] >= M and p["waves"] in (2, 3, 4, 6, 7), where
     elif p["kernel"] == 2:  # many-row kernel: bf16 weights only
         assert not fp8 and M > 64 and p["features"] in (256, 192, 128), where
         assert p["waves"] == (12 if p["features"] == 192 else 8), where
