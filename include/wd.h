@@ -203,14 +203,17 @@ wd_status wd_slide_window(wd_seq* s);
  * (WD_ERR_STATE otherwise); WD_ERR_UNSUPPORTED with adaptive termination. */
 wd_status wd_refresh_buffer(wd_seq* s);
 
-/* One diffusion step.  If a phase is due it slides and refreshes first.  On
- * the refresh step the active rows' logits come from the refresh forward; on
- * a normal step only the online rows (active positions and positions decoded
- * earlier in the phase) run the layer stack, overwrite their own K/V rows and
- * attend to all cached rows of [0, c).  Then logits on the active positions,
- * confidence (softmax probability of the argmax token, [MASK] excluded, ties
- * to the lowest id) and the unmask_per_step most confident positions are
- * decoded (ties to the lowest position).  `out` may be NULL (fully
+/* One diffusion step: the update of Sec. 3.1 (predict every candidate
+ * position, then decode the most confident ones), restricted to the active
+ * positions of the internal window (Sec. 4.2), with the two step roles of
+ * Sec. 4.3.  If a phase is due it slides and refreshes first (the refresh
+ * step of Sec. 4.3: its active rows' logits come from the refresh forward).
+ * On a normal step (Sec. 4.3) only the online rows (active positions and
+ * positions decoded earlier in the phase) run the layer stack, overwrite
+ * their own K/V rows and attend to all cached rows of [0, c).  Then logits
+ * on the active positions, confidence (softmax probability of the argmax
+ * token, [MASK] excluded, ties to the lowest id) and the unmask_per_step most
+ * confident positions are decoded (ties to the lowest position).  `out` may be NULL (fully
  * asynchronous); otherwise the call synchronizes the stream and fills it.
  * WD_ERR_STATE when every position is already decoded.  With adaptive
  * termination each unfinished sequence takes its own kind of step (a phase
@@ -235,7 +238,13 @@ wd_status wd_seq_ends(const wd_seq* s, int32_t* ends);
 
 /* Synchronizes, then copies the token ids (sum of sequence lengths, sequence
  * after sequence) and the step counter to the host.  `decoded` (same length,
- * 1 = decoded) may be NULL. */
+ * 1 = decoded) may be NULL.  Also reads the device's own checks of every step
+ * taken so far (the rows and active positions it derived from the decoded
+ * flags, each phase's retained prefix, and min(unmask_per_step, active)
+ * undecoded positions decoded per sequence and step, all against the host's
+ * schedule): WD_ERR_DEVICE, after the copies, if any of them failed.  A step
+ * called with out == NULL reports nothing itself, so a caller that never asks
+ * for step results learns of such a failure here. */
 wd_status wd_get_state(const wd_seq* s, int32_t* tokens, uint8_t* decoded, int32_t* t);
 
 /* on != 0: every later step also stores its active-row logits for

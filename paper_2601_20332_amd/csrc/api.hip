@@ -984,8 +984,10 @@ WdStepGeom base_geom(const wd_seq* s) {
   return g;
 }
 
-// LM head on the compact active rows, confidence, top-k decode.
-wd_status decide(wd_seq* s, int n_act) {
+// LM head on the compact active rows, confidence, top-k decode.  rows: the
+// step's per-sequence modes and active counts (NULL: every sequence has n_act
+// active positions), which the decode checks its picks against.
+wd_status decide(wd_seq* s, int n_act, const WdStepGeom* rows = nullptr) {
   const wd_model& m = *s->m;
   const wd_model_config& c = m.cfg;
   const int n = s->B * n_act;
@@ -1017,9 +1019,14 @@ wd_status decide(wd_seq* s, int n_act) {
                           s->conf_scratch, m.stream));
     s->logits_valid = true;
   }
-  const WdStepGeom g = base_geom(s);
+  WdStepGeom g = base_geom(s);
+  for (int b = 0; b < s->B; ++b) {
+    g.mode[b] = rows ? rows->mode[b] : 0;
+    g.nact[b] = rows ? rows->nact[b] : n_act;
+  }
   WD_HIP(wd::select_update(s->act_pos, s->act_tok, s->act_conf, n_act, s->win.unmask_per_step, g,
-                           s->seq_len, s->x, s->dec, s->sel_pos, s->sel_tok, s->sel_conf, m.stream));
+                           s->seq_len, s->x, s->dec, s->sel_pos, s->sel_tok, s->sel_conf, s->err,
+                           m.stream));
   s->last_nA = n_act;
   return WD_OK;
 }
@@ -1119,7 +1126,7 @@ wd_status step_tracked(wd_seq* s, wd_step_out* out, bool full) {
   r.M = row;
   r.n_act = stride;
   WD_TRY(forward(s, r));
-  WD_TRY(decide(s, stride));
+  WD_TRY(decide(s, stride, &r.g));
   const int step = s->t;
   s->t++;
   // the decisions, read back every step
@@ -1447,6 +1454,11 @@ wd_status wd_get_state(const wd_seq* s, int32_t* tokens, uint8_t* decoded, int32
   WD_HIP(hipMemcpy(tokens, s->x, s->T * 4, hipMemcpyDeviceToHost));
   if (decoded) WD_HIP(hipMemcpy(decoded, s->dec, s->T, hipMemcpyDeviceToHost));
   if (t) *t = s->t;
+  // the device's checks of every step so far against the host's schedule
+  int32_t err = 0;
+  WD_HIP(hipMemcpy(&err, s->err, 4, hipMemcpyDeviceToHost));
+  if (err != 0)
+    return fail(WD_ERR_DEVICE, "device bookkeeping disagrees with the schedule (code %d)", err);
   return WD_OK;
 }
 

@@ -316,6 +316,8 @@ hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, uint8_t* decoded_pre
 // ---- top-k decode -------------------------------------------------------------------------------
 // Candidate i of sequence b (index b * n_act + i) ranks by (conf desc,
 // position asc); the k best are decoded.
+// err bit 2: sequence b decoded other than min(k, g.nact[b]) positions, or a
+// candidate was already decoded (the host's schedule assumes neither).
 __global__ __launch_bounds__(256) void k_select_update(const int32_t* __restrict__ act_pos,
                                                        const int32_t* __restrict__ act_tok,
                                                        const float* __restrict__ act_conf,
@@ -325,7 +327,9 @@ __global__ __launch_bounds__(256) void k_select_update(const int32_t* __restrict
                                                        uint8_t* __restrict__ dec,
                                                        int32_t* __restrict__ sel_pos,
                                                        int32_t* __restrict__ sel_tok,
-                                                       float* __restrict__ sel_conf) {
+                                                       float* __restrict__ sel_conf,
+                                                       int32_t* __restrict__ err) {
+  __shared__ int n_sel, bad;
   const int b = blockIdx.x;
   const long base = (long)b * n_act;
   for (int i = threadIdx.x; i < k; i += blockDim.x) {
@@ -333,6 +337,7 @@ __global__ __launch_bounds__(256) void k_select_update(const int32_t* __restrict
     sel_tok[b * k + i] = -1;
     sel_conf[b * k + i] = 0.f;
   }
+  if (threadIdx.x == 0) n_sel = bad = 0;
   __syncthreads();
   const int S = seq_len[b];
   for (int i = threadIdx.x; i < n_act; i += blockDim.x) {
@@ -347,22 +352,30 @@ __global__ __launch_bounds__(256) void k_select_update(const int32_t* __restrict
       rank += (cj > ci) || (cj == ci && pj < pi);
     }
     if (rank < k) {
+      // each thread reads and writes only its own candidate's flag
+      if (dec[g.off[b] + pi]) atomicOr(&bad, 1);
       const int t = act_tok[base + i];
       sel_pos[b * k + rank] = pi;
       sel_tok[b * k + rank] = t;
       sel_conf[b * k + rank] = ci;
       x[g.off[b] + pi] = t;
       dec[g.off[b] + pi] = 1;
+      atomicAdd(&n_sel, 1);
     }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int want = g.mode[b] < 0 ? 0 : min(k, g.nact[b]);
+    if (bad || n_sel != want) atomicOr(err, 4);
   }
 }
 
 hipError_t select_update(const int32_t* act_pos, const int32_t* act_tok, const float* act_conf,
                          int n_act, int k, const WdStepGeom& g, const int32_t* seq_len, int32_t* x,
                          uint8_t* decoded, int32_t* sel_pos, int32_t* sel_tok, float* sel_conf,
-                         hipStream_t st) {
+                         int32_t* err, hipStream_t st) {
   hipLaunchKernelGGL(k_select_update, dim3(g.batch), dim3(256), 0, st, act_pos, act_tok, act_conf,
-                     n_act, k, g, seq_len, x, decoded, sel_pos, sel_tok, sel_conf);
+                     n_act, k, g, seq_len, x, decoded, sel_pos, sel_tok, sel_conf, err);
   return hipGetLastError();
 }
 

@@ -150,11 +150,13 @@ hipError_t build_rows(const uint8_t* decoded, const uint8_t* decoded0, const uin
 hipError_t slide(const uint8_t* decoded, uint8_t* decoded0, uint8_t* decoded_prev, int Smax, int E,
                  const WdStepGeom& g, const int32_t* seq_len, int32_t* err, hipStream_t st);
 // Top-k decode of each sequence among its n_act candidates; writes tokens,
-// decoded flags and the step's selection (b * k + rank).
+// decoded flags and the step's selection (b * k + rank).  Sets err bit 2
+// when sequence b (g.mode[b] >= 0) decodes other than min(k, g.nact[b])
+// positions or a candidate that is already decoded.
 hipError_t select_update(const int32_t* act_pos, const int32_t* act_tok, const float* act_conf,
                          int n_act, int k, const WdStepGeom& g, const int32_t* seq_len, int32_t* x,
                          uint8_t* decoded, int32_t* sel_pos, int32_t* sel_tok, float* sel_conf,
-                         hipStream_t st);
+                         int32_t* err, hipStream_t st);
 // Utility: widen n dtype elements (strided rows) to fp32.
 template <typename T>
 hipError_t widen_rows(const T* src, long src_stride, float* dst, int rows, int cols, hipStream_t st);

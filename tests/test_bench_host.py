@@ -35,6 +35,7 @@ SPLIT = "void wd::k_gemm_bf16<1, 3, 8, 8, false>(unsigned short const*, int)"
 DMA = "void wd::k_gemm_bf16_dma<3, 4, true, 12, 6>(unsigned short const*, int)"
 BIG = "void wd::k_gemm_bf16_big<2, false>(unsigned short const*, int)"
 ATTN = "wd::k_attn_bf16(unsigned short const*, int)"
+COMBINE = "wd::k_attn_combine(float const*, int)"
 COPY = "__amd_rocclr_copyBuffer"
 
 
@@ -43,7 +44,9 @@ def test_kernel_classes():
     assert bench.kernel_class_of(SPLIT) == 1
     assert bench.kernel_class_of(DMA) == 2
     assert bench.kernel_class_of(BIG) == 2
-    assert bench.kernel_class_of(ATTN) is None
+    assert bench.kernel_class_of(ATTN) == 4
+    assert bench.kernel_class_of(COMBINE) == 4
+    assert bench.starts_unit(ATTN) and not bench.starts_unit(COMBINE) and bench.starts_unit(DMA)
     assert bench.kernel_class_of(COPY) is None
 
 
@@ -53,19 +56,24 @@ def test_pmc_summary_scales_counts_by_the_copy(tmp_path, monkeypatch):
     # a 1 MiB copy reads 2048 and writes 1024 counts: 512 and 1024 bytes per count
     cf = _counter_folder(tmp_path / "cf", [(COPY, 2048.0), (COPY, 2048.0)])
     cw = _counter_folder(tmp_path / "cw", [(COPY, 1024.0)])
+    # two attention units: one with a split merge, one without
     gf = _counter_folder(tmp_path / "gf", [(FUSED, 100.0), (SPLIT, 300.0), (DMA, 1000.0),
-                                           (ATTN, 7.0)])
+                                           (ATTN, 7.0), (COMBINE, 3.0), (ATTN, 5.0)])
     gw = _counter_folder(tmp_path / "gw", [(FUSED, 2.0), (SPLIT, 6.0), (DMA, 40.0),
-                                           (ATTN, 7.0)])
+                                           (ATTN, 1.0), (COMBINE, 2.0), (ATTN, 1.0)])
     bench.pmc_summary(gf, gw, cf, cw, copy_mib=1)
     rec = json.loads(traffic.read_text())
-    assert rec["gemm_source_sha256_16"] == bench.gemm_source_hash()
     assert rec["fetch_bytes_per_count"] == 512.0 and rec["write_bytes_per_count"] == 1024.0
     few, many = rec["kernels"]["k_gemm_bf16"], rec["kernels"]["k_gemm_bf16_dma"]
+    attn = rec["kernels"]["k_attn_bf16"]
+    assert few["source_sha256_16"] == bench.source_hash("k_gemm_bf16")
+    assert attn["source_sha256_16"] == bench.source_hash("k_attn_bf16")
     assert few["dispatches"] == 2 and many["dispatches"] == 1
     assert few["hbm_fetch_bytes_per_launch"] == round((100 + 300) / 2 * 512)
     assert few["hbm_write_bytes_per_launch"] == round((2 + 6) / 2 * 1024)
     assert many["hbm_bytes_per_launch"] == round(1000 * 512 + 40 * 1024)
+    assert attn["units"] == 2 and attn["dispatches"] == 3
+    assert attn["hbm_bytes_per_launch"] == round((7 + 3 + 5) / 2 * 512 + (1 + 2 + 1) / 2 * 1024)
 
 
 def test_pmc_summary_rejects_unpaired_runs(tmp_path, monkeypatch):
@@ -81,14 +89,18 @@ def test_pmc_summary_rejects_unpaired_runs(tmp_path, monkeypatch):
 def test_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
     traffic = tmp_path / "traffic.json"
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(traffic))
-    rec = {"gemm_source_sha256_16": bench.gemm_source_hash(),
-           "kernels": {"k_gemm_bf16": {"hbm_bytes_per_launch": 123}}}
+    rec = {"kernels": {"k_gemm_bf16": {"hbm_bytes_per_launch": 123,
+                                       "source_sha256_16": bench.source_hash("k_gemm_bf16")},
+                       "k_attn_bf16": {"hbm_bytes_per_launch": 77,
+                                       "source_sha256_16": bench.source_hash("k_attn_bf16")}}}
     traffic.write_text(json.dumps(rec))
     assert bench.measured_traffic("k_gemm_bf16") == 123
+    assert bench.measured_traffic("k_attn_bf16") == 77
     assert bench.measured_traffic("k_gemm_bf16_dma") is None
-    rec["gemm_source_sha256_16"] = "0" * 16
+    rec["kernels"]["k_gemm_bf16"]["source_sha256_16"] = "0" * 16
     traffic.write_text(json.dumps(rec))
     assert bench.measured_traffic("k_gemm_bf16") is None
+    assert bench.measured_traffic("k_attn_bf16") == 77
     traffic.write_text("not json")
     assert bench.measured_traffic("k_gemm_bf16") is None
 

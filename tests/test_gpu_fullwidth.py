@@ -57,6 +57,77 @@ def test_first_phases_at_full_width(name, n_steps, seqs):
         assert rep.steps == n_steps
 
 
+def test_llada8b_2_layers_pruning_only():
+    """R = 1 with E = 96 < G = 256 at the LLaDA-8B width (the pruning-only
+    setting of Table 1, Sec. 5.2): every step is a refresh over [0, c)."""
+    w = synth.WORKLOADS["llada8b"]
+    shape = synth.with_layers(w.model, 2)
+    win = synth.WindowSettings(w.window.n_active, w.window.n_buffer, 1, 1)
+    n_steps = 6
+    log("[case] llada8b at full width, 2 layers, R = 1, E = 96")
+    W = synth.Weights(shape)
+    m = gpu_model(W)
+    prompts = synth.prompts(shape, [w.prompt_len])
+    steps, _ = run_gpu(m, prompts, w.gen_len, win, max_steps=n_steps)
+    m.free()
+    assert all(s.res.is_refresh for s in steps)
+    assert [s.res.n_rows for s in steps] == [w.prompt_len + 96 + t for t in range(n_steps)]
+    rep = check_sequence(OracleModel(W, cache_budget_bytes=40e9), prompts[0], w.gen_len, win,
+                         steps, 0, 1, max_steps=n_steps)
+    print(f"PARITY llada8b-2L-R1 seq=0 steps={rep.steps} max_rel_logit_err={rep.max_rel:.3e} "
+          f"adopted_sel={rep.select_adopted} adopted_tok={rep.token_adopted}", flush=True)
+    assert rep.steps == n_steps
+
+
+class HeldWeights(synth.Weights):
+    """Seeded weights generated once and kept as drawn (bf16 bit patterns), so
+    the GPU upload and the oracle read the same draw without generating the
+    8B parameters twice."""
+
+    def __init__(self, *a, **k):
+        super().__init__(*a, **k)
+        self._held = {}
+
+    def raw(self, i):
+        r = self._held.get(i)
+        if r is None:
+            r = self._held[i] = super().raw(i)
+        return r
+
+    def drop(self):
+        self._held.clear()
+
+
+@pytest.mark.timeout(900)
+def test_llada8b_full_depth_against_oracle():
+    """All 32 layers of the LLaDA-8B workload at its window settings: the first
+    refresh step, the phase's 7 normal steps and the next refresh step (R + 1
+    steps) against the float64 oracle, so the bf16 bound is checked at the
+    depth the benchmark runs, where rounding differences accumulate over the
+    layers (Sec. 4.3 refresh and normal steps, Sec. 5.1 model)."""
+    w = synth.WORKLOADS["llada8b"]
+    shape = w.model
+    n_steps = w.window.refresh_every + 1
+    t0 = time.time()
+    log(f"[case] llada8b full depth ({shape.n_layers} layers), {n_steps} steps against the oracle")
+    W = HeldWeights(shape)
+    m = gpu_model(W)
+    prompts = synth.prompts(shape, [w.prompt_len])
+    steps, _ = run_gpu(m, prompts, w.gen_len, w.window, max_steps=n_steps)
+    m.free()
+    log(f"[gpu] {len(steps)} steps, weights drawn and run in {time.time() - t0:.1f}s")
+    # every float64 weight stays resident: 8.0e9 parameters x 8 bytes
+    om = OracleModel(W, cache_budget_bytes=80e9)
+    rep = check_sequence(om, prompts[0], w.gen_len, w.window, steps, 0, 1, max_steps=n_steps,
+                         progress=True)
+    W.drop()
+    print(f"PARITY llada8b-32L seq=0 steps={rep.steps} max_rel_logit_err={rep.max_rel:.3e} "
+          f"adopted_sel={rep.select_adopted} adopted_tok={rep.token_adopted} "
+          f"({time.time() - t0:.1f}s)", flush=True)
+    assert rep.steps == n_steps
+    assert steps[0].res.is_refresh and steps[-1].res.is_refresh
+
+
 def test_llada8b_32_layers_window_covering_everything_equals_full_path():
     """With E >= G, n_active >= G and R = 1 Window-Diffusion is standard decoding;
     on the GPU both paths run the same row sets through the same kernels, so the

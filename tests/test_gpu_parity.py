@@ -123,6 +123,18 @@ def test_bf16_edge_windows():
         _run_and_check(MICRO_MHA, prompts, 10, win)
 
 
+def test_bf16_pruning_only_every_step_refreshes():
+    """Window pruning without the cache (the Table 1 setting of Sec. 5.2): R =
+    1, so every step is a refresh over the retained prefix [0, c), with E = 8
+    well below G = 24 (far-field positions pruned at every step)."""
+    prompts = synth.prompts(MICRO_GQA, [17, 40])
+    steps, _, _ = _run_and_check(MICRO_GQA, prompts, 24, synth.WindowSettings(4, 4, 1, 1))
+    assert all(s.res.is_refresh for s in steps)
+    # rows = c = the E-th undecoded position + 1, per sequence: below S until
+    # fewer than E undecoded positions remain
+    assert steps[0].res.n_rows == (17 + 8) + (40 + 8)
+
+
 @pytest.mark.parametrize("dtype_shape", [synth.WORKLOADS["tiny"].model, MICRO_GQA])
 def test_refresh_cache_equals_oracle_kv(dtype_shape):
     """After a refresh step the cache holds K/V of the forward over [0, c)."""

@@ -11,8 +11,14 @@ rank differently only if |log c_i - log c_j| <= 2 (d_i + d_j).  Inside that
 band the oracle adopts the GPU's choice, which must itself be the top-k of
 the GPU's own logits.  fp32 models must match with no adoption.  A decoded
 token must equal the oracle's wherever the oracle's top-1 logit margin
-exceeds 1e-2, and is adopted otherwise.  Adoptions are counted; callers bound
-them.
+exceeds 1e-2, and is adopted otherwise.  Adoptions are counted and bounded
+here: none at all for fp32 models, and for bf16 models at most
+MAX_ADOPT_FRAC of the checked steps (callers may pass a tighter bound).  On
+random-init models with vocabularies of a few thousand entries the
+confidences are nearly flat, so band adoptions are common (up to 53% of the
+steps measured on a 2048-entry micro model); a kernel that systematically
+misranks would exceed the bound even where each single choice stays inside
+its band.
 """
 from __future__ import annotations
 
@@ -29,6 +35,7 @@ from oracle.schedule import FullDecoder, WindowedDecoder
 
 LOGIT_TOL = {synth.DTYPE_F32: 1e-4, synth.DTYPE_BF16: 2e-2}
 MARGIN = 1e-2
+MAX_ADOPT_FRAC = 0.6
 
 
 def log(*a):
@@ -51,9 +58,12 @@ def gpu_model(W: synth.Weights, device="cuda", weight_fp8: bool = False):
     import torch
     import paper_2601_20332_amd as wd
     ts = []
-    for _, raw in W.iter_raw(workers=8):
+    n = len(W.specs)
+    for i, raw in W.iter_raw(workers=8):
         a = raw.view(np.int16) if raw.dtype == np.uint16 else raw
         ts.append(torch.from_numpy(np.ascontiguousarray(a)).to(device))
+        if n > 100 and (i + 1) % 64 == 0:
+            log(f"[weights] {i + 1}/{n} tensors uploaded")
     m = wd.wd_init_model(cfg_of(W.shape, weight_fp8), ts, device)
     del ts
     return m
@@ -108,13 +118,15 @@ class Report:
 
 
 def rel_err(g: np.ndarray, o: np.ndarray) -> np.ndarray:
-    return np.abs(g - o).max(axis=1) / np.abs(o).max(axis=1)
+    """Per row max|g - o| / max|o| (an all-zero oracle row must be matched exactly)."""
+    return np.abs(g - o).max(axis=1) / np.maximum(np.abs(o).max(axis=1), 1e-300)
 
 
 def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuStep], b: int,
                    batch: int, full: bool = False, max_steps: Optional[int] = None,
                    eos_id: Optional[int] = None, gpu_end: Optional[int] = None,
-                   refresh: str = "full") -> Report:
+                   refresh: str = "full", max_adopt_frac: float = MAX_ADOPT_FRAC,
+                   progress: bool = False) -> Report:
     """Replays sequence b of a GPU generation in the oracle and compares every step.
     With eos_id, a sequence the oracle has finished must have no active row and
     no decision on the GPU either, and the live ends must agree."""
@@ -178,6 +190,14 @@ def check_sequence(om: OracleModel, prompt, gen_len, win, gpu_steps: List[GpuSte
 
         dec.step(override=override, keep_logits=True)
         rep.steps += 1
+        if progress:
+            log(f"[oracle] step {t} checked: max rel logit err so far {rep.max_rel:.3e}, "
+                f"adopted {rep.select_adopted} selections, {rep.token_adopted} tokens")
+    frac = 0.0 if dtype == synth.DTYPE_F32 else max_adopt_frac
+    assert rep.select_adopted <= frac * rep.steps, (
+        f"sequence {b}: {rep.select_adopted} of {rep.steps} selections adopted (bound {frac})")
+    assert rep.token_adopted <= frac * rep.steps * win.unmask_per_step, (
+        f"sequence {b}: {rep.token_adopted} tokens adopted over {rep.steps} steps (bound {frac})")
     if max_steps is None:
         assert dec.done(), f"sequence {b}: the GPU stopped before the oracle finished"
     if gpu_end is not None:
