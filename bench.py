@@ -17,8 +17,11 @@ events on the library's stream; HBM bound), the same for the many-row GEMM
 of the refresh steps (k_gemm_bf16_dma; MFMA bound), adaptive termination at
 <eos> on the same workload (an <eos> id taken from the fixed-length run), the
 buffer-only refresh variant (not the paper's method), the FP8-weight variant
-(not the paper's precision) and the CPU oracle on a bounded sample of the same
-workload.
+(not the paper's precision), the same model on the long generation (512 +
+1024, with its full-sequence comparison) and on the ragged batch of 16, the
+Dream-7B shape, and the CPU oracle on a bounded sample of the same workload.
+Every generation ends with a read of the device's own checks of its steps;
+a failed check raises, so no record is printed for it.
 """
 from __future__ import annotations
 
@@ -35,45 +38,61 @@ sys.path.insert(0, ROOT)
 METRIC = "denoising steps/s + decoded tokens/s at LLaDA-8B shape, 1 GPU; MFMA/HBM % peak"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_traffic.json")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2601_20332_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kernel_traffic.json")
+CSRC = os.path.join(ROOT, "paper_2601_20332_amd", "csrc")
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def gemm_source_hash() -> str:
-    return hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+# kernel classes of wd_profile_read, the kernel each one is named by, and the
+# source file that holds it (its hash gates the stored counter traffic)
+KERNEL_CLASSES = {1: "k_gemm_bf16", 2: "k_gemm_bf16_dma", 4: "k_attn_bf16"}
+PROFILE_NAMES = KERNEL_CLASSES
+KERNEL_SOURCES = {"k_gemm_bf16": "gemm.hip", "k_gemm_bf16_dma": "gemm.hip",
+                  "k_attn_bf16": "layer.hip"}
 
 
-# GEMM kernel classes of wd_profile_read and the kernel each one is
-KERNEL_CLASSES = {1: "k_gemm_bf16", 2: "k_gemm_bf16_dma"}
-PROFILE_NAMES = {**KERNEL_CLASSES, 4: "k_attn_bf16"}
+def source_hash(kernel: str) -> str:
+    path = os.path.join(CSRC, KERNEL_SOURCES[kernel])
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
 def measured_traffic(kernel: str):
-    """HBM bytes per launch of one GEMM kernel from the committed rocprofv3 counter
-    runs, if they were taken on the current kernel source."""
+    """HBM bytes per launch (per unit for attention) of one kernel class from the
+    committed rocprofv3 counter runs, if they were taken on the current source
+    of that kernel."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if rec.get("gemm_source_sha256_16") != gemm_source_hash():
+    k = rec.get("kernels", {}).get(kernel, {})
+    if not k or k.get("source_sha256_16") != source_hash(kernel):
         return None
-    return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
+    return k.get("hbm_bytes_per_launch")
 
 
 def kernel_class_of(name: str):
     """WD_PROF_* class of a kernel name as rocprofv3 prints it: the few-row
     products (k_gemm_bf16, and k_gemm_bf16_fused that carries the Q/K/V or
-    SwiGLU epilogue) or the many-row kernels (k_gemm_bf16_dma; k_gemm_bf16_big
-    where the former does not apply: fp8 weights, widths not a multiple of 256)."""
+    SwiGLU epilogue), the many-row kernels (k_gemm_bf16_dma; k_gemm_bf16_big
+    where the former does not apply: fp8 weights, widths not a multiple of
+    256), or one layer's bf16 attention (k_attn_bf16 and its split merge
+    k_attn_combine)."""
     if "k_gemm_bf16_dma<" in name or "k_gemm_bf16_big<" in name:
         return 2
     if "k_gemm_bf16<" in name or "k_gemm_bf16_fused<" in name:
         return 1
+    if "k_attn_bf16" in name or "k_attn_combine" in name:
+        return 4
     return None
+
+
+def starts_unit(name: str) -> bool:
+    """Whether a dispatch starts a timing unit: every GEMM launch does; an
+    attention unit is k_attn_bf16 plus the k_attn_combine that may follow it."""
+    return "k_attn_combine" not in name
 
 
 def read_counter_csv(folder: str):
@@ -95,7 +114,8 @@ def pmc_summary(gemm_fetch: str, gemm_write: str, copy_fetch: str, copy_write: s
                 copy_mib: int):
     """Turn the four rocprofv3 counter runs (FETCH_SIZE and WRITE_SIZE, in KiB per
     dispatch, over one generation and over plain copies of copy_mib MiB) into HBM
-    bytes per launch of each GEMM kernel; writes TRAFFIC_FILE and prints a table."""
+    bytes per launch of each GEMM kernel and per layer of attention; writes
+    TRAFFIC_FILE and prints a table."""
     copy_bytes = copy_mib << 20
 
     def copy_scale(folder):
@@ -112,8 +132,10 @@ def pmc_summary(gemm_fetch: str, gemm_write: str, copy_fetch: str, copy_write: s
             if cls is None:
                 continue
             k = KERNEL_CLASSES[cls]
-            d = per.setdefault(k, {"fetch": [], "write": [], "instances": {}})
+            d = per.setdefault(k, {"fetch": [], "write": [], "fetch_units": 0, "write_units": 0,
+                                   "instances": {}})
             d[key].append(v * scale)
+            d[key + "_units"] += starts_unit(name)
             inst = name.split("(")[0].replace("void ", "")
             di = d["instances"].setdefault(inst, {"fetch": [], "write": []})
             di[key].append(v * scale)
@@ -121,17 +143,19 @@ def pmc_summary(gemm_fetch: str, gemm_write: str, copy_fetch: str, copy_write: s
     lines = ["| kernel instance | dispatches | fetched MB / dispatch | written MB / dispatch |",
              "|---|---|---|---|"]
     for k, d in per.items():
-        if len(d["fetch"]) != len(d["write"]):
+        if len(d["fetch"]) != len(d["write"]) or d["fetch_units"] != d["write_units"]:
             sys.exit(f"{k}: {len(d['fetch'])} FETCH_SIZE vs {len(d['write'])} WRITE_SIZE dispatches")
-        n = len(d["fetch"])
+        n = d["fetch_units"]
         f, w = sum(d["fetch"]) / n, sum(d["write"]) / n
-        kernels[k] = {"dispatches": n, "hbm_fetch_bytes_per_launch": round(f),
+        kernels[k] = {"source": KERNEL_SOURCES[k], "source_sha256_16": source_hash(k),
+                      "dispatches": len(d["fetch"]), "units": n,
+                      "hbm_fetch_bytes_per_launch": round(f),
                       "hbm_write_bytes_per_launch": round(w), "hbm_bytes_per_launch": round(f + w)}
         for inst, di in sorted(d["instances"].items(), key=lambda x: -len(x[1]["fetch"])):
             m = len(di["fetch"])
             lines.append(f"| `{inst}` | {m} | {sum(di['fetch']) / m / 1e6:.1f} | "
                          f"{sum(di['write']) / max(1, len(di['write'])) / 1e6:.2f} |")
-    rec = {"gemm_source_sha256_16": gemm_source_hash(), "copy_mib": copy_mib,
+    rec = {"copy_mib": copy_mib,
            "fetch_bytes_per_count": round(sf, 4), "write_bytes_per_count": round(sw, 4),
            "kernels": kernels}
     with open(TRAFFIC_FILE, "w") as fh:
@@ -235,43 +259,52 @@ def fp8_weight_variant(model8, prompts, w, n_steps, fixed_s):
     }
 
 
-def other_workload(name: str, device: str):
-    """Windowed generation on a second workload shape (one model upload, one
-    warm-up, two timed generations, one full-sequence generation for the
-    speedup, one instrumented generation for the GEMM rooflines)."""
+def other_workload(name: str, device: str, model=None, reps: int = 2, warm: bool = True,
+                   full: bool = True):
+    """Windowed generation on another workload: one model upload (or `model`,
+    already packed, when the workload has the same model shape), one warm-up
+    (`warm`), `reps` timed generations, one full-sequence generation for the
+    speedup (`full`), one instrumented generation for the kernel rooflines."""
     import paper_2601_20332_amd as wd
     import synth
     import torch
     w = synth.WORKLOADS[name]
-    t0 = time.time()
-    model = upload_model(w.model, device)
-    log(f"[bench] {name}: weights generated and packed in {time.time() - t0:.1f}s")
+    own = model is None
+    if own:
+        t0 = time.time()
+        model = upload_model(w.model, device)
+        log(f"[bench] {name}: weights generated and packed in {time.time() - t0:.1f}s")
     prompts = synth.prompts(w.model, synth.prompt_lengths(w))
     win = w.window
     wc = wd.window_config(win.n_active, win.n_buffer, win.refresh_every, win.unmask_per_step)
     n_steps = len(wd.wd_plan(w.prompt_len, w.gen_len, wc)["n_rows"])
-    generation(model, prompts, w.gen_len, wc, n_steps)
-    torch.cuda.synchronize()
-    reps = 2
-    t1 = time.perf_counter()
-    for _ in range(reps):
+    if warm:
         generation(model, prompts, w.gen_len, wc, n_steps)
     torch.cuda.synchronize()
-    t = (time.perf_counter() - t1) / reps
-    tf = time.perf_counter()
-    generation(model, prompts, w.gen_len, wc, n_steps, full=True)
+    t1 = time.perf_counter()
+    for _ in range(reps):
+        generation(model, prompts, w.gen_len, wc, n_steps, progress=128)
     torch.cuda.synchronize()
-    t_full = time.perf_counter() - tf
+    t = (time.perf_counter() - t1) / reps
+    log(f"[bench] {name}: {reps} timed generations, {t:.3f}s each")
+    t_full = None
+    if full:
+        tf = time.perf_counter()
+        generation(model, prompts, w.gen_len, wc, n_steps, full=True, progress=128)
+        torch.cuda.synchronize()
+        t_full = time.perf_counter() - tf
+        log(f"[bench] {name}: full-sequence generation {t_full:.3f}s")
     wd.wd_profile_enable(model, True)
     te = time.perf_counter()
-    generation(model, prompts, w.gen_len, wc, n_steps)
+    generation(model, prompts, w.gen_len, wc, n_steps, progress=128)
     torch.cuda.synchronize()
     te = time.perf_counter() - te
     rows = roofline_of(model, wd.WD_PROF_GEMM_ROWS, te)
     tiled = roofline_of(model, wd.WD_PROF_GEMM_TILED, te)
     attn = roofline_of(model, wd.WD_PROF_ATTN, te)
     wd.wd_profile_enable(model, False)
-    model.free()
+    if own:
+        model.free()
     for r in (rows, tiled, attn):
         if r:
             r["traffic"] = None  # the counter runs cover the LLaDA-8B workload
@@ -281,13 +314,15 @@ def other_workload(name: str, device: str):
         "workload": (f"{name}: {m.n_layers}L hidden {m.hidden} {m.n_heads}q/{m.n_kv_heads}kv x "
                      f"{m.head_dim} ffn {m.ffn} vocab {m.vocab}{' qkv bias' if m.qkv_bias else ''}, "
                      f"random init N(0,0.02)"),
-        "batch": B, "prompt_len": w.prompt_len, "gen_len": w.gen_len,
+        "batch": B, "prompt_len": w.prompt_len if B == 1 else synth.prompt_lengths(w),
+        "gen_len": w.gen_len,
         "n_active": win.n_active, "n_buffer": win.n_buffer, "refresh_every": win.refresh_every,
         "unmask_per_step": win.unmask_per_step,
+        "timed_generations": reps,
         "steps_per_s": round(n_steps / t, 3),
         "decoded_tokens_per_s": round(B * w.gen_len / t, 3),
         "ms_per_generation": round(t * 1e3, 2),
-        "speedup_vs_full_sequence": round(t_full / t, 3),
+        "speedup_vs_full_sequence": round(t_full / t, 3) if t_full else None,
         "roofline": rows,
         "roofline_tiled_gemm": tiled,
         "roofline_attention": attn,
@@ -304,7 +339,12 @@ def generation(model, prompts, G, wc, n_steps, full=False, progress=None):
         wd._check(fn(gen.handle, None))
         if progress and (i + 1) % progress == 0:
             log(f"[bench] {'full-sequence' if full else 'windowed'} step {i + 1}/{n_steps}")
-    gen.free()  # synchronizes the stream
+    # synchronizes; raises if the device's checks of any step against the
+    # host's schedule failed, so a generation that went wrong gives no record
+    _, decoded, t = wd.wd_get_state(gen)
+    gen.free()
+    if t != n_steps or not all(d.all() for d in decoded):
+        raise RuntimeError(f"generation ended after {t} steps with undecoded positions")
 
 
 def run_until_done(model, prompts, G, wc):
@@ -323,7 +363,8 @@ def run_until_done(model, prompts, G, wc):
         wd._check(st)
         n += 1
     ends = [int(e) for e in wd.wd_seq_ends(gen)]
-    gen.free()  # synchronizes the stream
+    wd.wd_get_state(gen)  # raises if the device's checks failed
+    gen.free()
     return n, time.perf_counter() - t0, ends
 
 
@@ -404,6 +445,19 @@ def buffer_refresh_variant(model, prompts, w, n_steps, fixed_s):
     }
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or the platform's string."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(w, plan, L_s=4, reps=20, ref_reps=10):
     """The float64 oracle on a bounded sample of the workload: after one untimed
     refresh forward (first-touch of its buffers), the mean of `ref_reps` refresh
@@ -459,6 +513,8 @@ def cpu_baseline(w, plan, L_s=4, reps=20, ref_reps=10):
         "value": len(plan) / total,
         "unit": "steps/s",
         "cores": int(threads),
+        "cpu_model": cpu_model(),
+        "host_cpus_available": len(os.sched_getaffinity(0)),
         "kind": "oracle",
         "sample": (f"float64 oracle, {L_s} of {L} layers: refresh forward over {c_ref} rows "
                    f"({(t1 - t0) / ref_reps:.1f} s, mean of {ref_reps}), normal-step forward over {m_norm} rows "
@@ -494,8 +550,9 @@ def main():
     ap.add_argument("--pmc-summary", nargs=4, metavar=("GEMM_FETCH", "GEMM_WRITE", "COPY_FETCH",
                                                         "COPY_WRITE"),
                     help="only turn four rocprofv3 --pmc csv folders into HBM bytes per GEMM "
-                         "launch (copies of --calibrate-copy MiB, default 1024), write "
-                         "profiles/gemm_bf16_traffic.json and exit; needs no GPU")
+                         "launch and per layer of attention (copies of --calibrate-copy MiB, "
+                         "default 1024), write profiles/kernel_traffic.json and exit; needs "
+                         "no GPU")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary, copy_mib=args.calibrate_copy or 1024)
@@ -606,17 +663,29 @@ def main():
             if r:
                 meas = gbs_meas if r["unit"] == "GB/s" else tf_meas
                 r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
-    model.free()
     others = None
     if not args.no_others and args.workload == "llada8b":
-        others = {"dream7b": other_workload("dream7b", device)}
+        others = {}
+        # the same LLaDA-8B model: the long generation (Sec. 5.3, time against
+        # generation length), with its full-sequence comparison, and the
+        # ragged batch of 16 (windowed only: its full-sequence leg alone takes
+        # about two minutes)
+        others["llada8b_long"] = other_workload("llada8b_long", device, model=model, reps=2,
+                                                warm=False)
+        log(f"[bench] llada8b_long: {others['llada8b_long']}")
+        others["llada8b_batch16"] = other_workload("llada8b_batch16", device, model=model, reps=1,
+                                                   warm=False, full=False)
+        log(f"[bench] llada8b_batch16: {others['llada8b_batch16']}")
+    model.free()
+    if others is not None:
+        others["dream7b"] = other_workload("dream7b", device)
         log(f"[bench] dream7b: {others['dream7b']}")
         if peaks:
-            for r in (others["dream7b"]["roofline"], others["dream7b"]["roofline_tiled_gemm"],
-                      others["dream7b"]["roofline_attention"]):
-                if r:
-                    meas = peaks["hbm_read_gbs"] if r["unit"] == "GB/s" else peaks["mfma_bf16_tflops"]
-                    r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
+            for o in others.values():
+                for r in (o["roofline"], o["roofline_tiled_gemm"], o["roofline_attention"]):
+                    if r:
+                        meas = peaks["hbm_read_gbs"] if r["unit"] == "GB/s" else peaks["mfma_bf16_tflops"]
+                        r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
 
     cpu = None
     if not args.no_cpu_baseline:
