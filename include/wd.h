@@ -222,6 +222,25 @@ wd_status wd_refresh_buffer(wd_seq* s);
  * WD_ERR_STATE once every sequence is finished. */
 wd_status wd_step(wd_seq* s, wd_step_out* out);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the step
+ * of wd_step, with the same kernels, launch plans and results, whose scratch
+ * (split-K partials of the projections, split-KV attention partials,
+ * confidence partials) lives in one static device array of the library,
+ * WD_STATIC_SCRATCH_BYTES per GPU, held from the library's first use on that
+ * GPU (wd_init_model resolves its address) until the process ends.  The call
+ * allocates nothing and calls no allocating routine.  Before running it
+ * bounds the step's scratch from its row counts and returns
+ * WD_ERR_OUT_OF_MEMORY, with the sequence untouched, when the bound exceeds
+ * the array (wd_step then takes the step).  Nothing in the array has to
+ * start at zero; every step writes what it reads.  All calls on one GPU share
+ * the array: calls that overlap in time on one GPU (other threads, other
+ * streams) race.  WD_ERR_UNSUPPORTED with adaptive termination or while
+ * kernel timing is enabled (it creates HIP events); otherwise the statuses
+ * of wd_step. */
+#define WD_STATIC_SCRATCH_BYTES ((size_t)96 << 20)
+wd_status wd_step_noalloc(wd_seq* s, wd_step_out* out);
+
 /* Standard decoding step (Sec. 3.1) for comparison: a forward over every
  * position of every sequence, logits for every undecoded position, and the
  * unmask_per_step most confident of them decoded.  With adaptive

@@ -31,7 +31,7 @@ EXPORTED = ["wd_weight_count", "wd_weight_shape", "wd_model_bytes", "wd_init_mod
             "wd_refresh_buffer", "wd_step", "wd_full_step", "wd_get_state", "wd_debug_logits",
             "wd_debug_kv", "wd_free_seq", "wd_plan", "wd_last_error", "wd_profile_enable",
             "wd_profile_read", "wd_seq_ends", "wd_debug_weight_row", "wd_debug_keep_logits", "wd_measure_peaks",
-            "wd_debug_gemm_plan"]
+            "wd_debug_gemm_plan", "wd_step_noalloc"]
 
 
 class WdError(RuntimeError):
@@ -94,6 +94,7 @@ def _load() -> ctypes.CDLL:
         "wd_slide_window": (i32, [P]),
         "wd_refresh_buffer": (i32, [P]),
         "wd_step": (i32, [P, ctypes.POINTER(StepOut)]),
+        "wd_step_noalloc": (i32, [P, ctypes.POINTER(StepOut)]),
         "wd_full_step": (i32, [P, ctypes.POINTER(StepOut)]),
         "wd_get_state": (i32, [P, pi32, ctypes.POINTER(ctypes.c_uint8), pi32]),
         "wd_seq_ends": (i32, [P, pi32]),
@@ -277,6 +278,11 @@ def _step(fn, gen: Generation, want: bool) -> Optional[StepResult]:
 
 def wd_step(gen: Generation, want_result: bool = True) -> Optional[StepResult]:
     return _step(lib.wd_step, gen, want_result)
+
+
+def wd_step_noalloc(gen: Generation, want_result: bool = True) -> Optional[StepResult]:
+    """wd_step with its scratch in the library's static device array (no allocation)."""
+    return _step(lib.wd_step_noalloc, gen, want_result)
 
 
 def wd_full_step(gen: Generation, want_result: bool = True) -> Optional[StepResult]:

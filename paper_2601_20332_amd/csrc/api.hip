@@ -16,12 +16,30 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
 #include "../../include/wd.h"
 #include "common.h"
 #include "kernels.h"
+
+// ---- scratch of the entry point that allocates nothing (wd_step_noalloc) -------------
+// The step's split-K partials, split-KV attention partials and confidence
+// partials live here instead of in the caller's workspace.  Each GPU the
+// library runs on holds its own copy until the process ends.  Host code must
+// not use the array's name (a host-side stand-in, not a device address): it
+// uses the address hipGetSymbolAddress gave for the device, kept per device.
+constexpr size_t kStaticScratchBytes = WD_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};  // device address of `scratch` on each device
+
+}  // namespace
 
 namespace {
 
@@ -51,6 +69,22 @@ wd_status fail(wd_status st, const char* fmt, ...) {
   } while (0)
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Resolves the device address of `scratch` on `device`, which must be the
+// current device; once per device.
+wd_status init_static_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices)
+    return fail(WD_ERR_UNSUPPORTED, "device %d beyond the %d the library tracks", device, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[device]) return WD_OK;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || !p)
+    return fail(WD_ERR_DEVICE, "hipGetSymbolAddress(scratch) failed on device %d: %s", device,
+                hipGetErrorString(e));
+  g_scratch_dev[device] = p;
+  return WD_OK;
+}
 
 // -- model shape checks --------------------------------------------------------------
 bool cfg_valid(const wd_model_config* c, std::string* why) {
@@ -409,6 +443,10 @@ wd_status wd_init_model(const wd_model_config* cfg, const void* const* weights, 
   if (hipGetDevice(&m->device) != hipSuccess) {
     delete m;
     return fail(WD_ERR_DEVICE, "hipGetDevice failed");
+  }
+  if (const wd_status ss = init_static_scratch(m->device); ss != WD_OK) {
+    delete m;
+    return ss;
   }
   m->esz = cfg->dtype == WD_DTYPE_BF16 ? 2 : 4;
   m->qkv_n = (cfg->n_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
@@ -887,6 +925,36 @@ bool fused_rows(const wd_model& m, int M, int N, int K, int epi) {
 
 wd_model& m_mut(wd_seq* s) { return *s->m; }
 
+// Which kernels a layer's products take at M rows.  Q/K/V: the fused few-row
+// kernel writes q and the cache itself; otherwise split-K partials and
+// k_qkv_epilogue.
+bool qkv_fused(const wd_model& m, int M) {
+  return fused_rows(m, M, m.qkv_n, m.cfg.hidden, wd::kEpiQkv);
+}
+// gate/up: 0 = the fused few-row kernel with SwiGLU, 1 = the many-row kernel
+// with SwiGLU in its epilogue (no K split), 2 = split-K partials and k_swiglu.
+int gateup_path(const wd_model& m, int M) {
+  const int F = m.cfg.ffn, H = m.cfg.hidden;
+  if (fused_rows(m, M, 2 * F, H, wd::kEpiSwiGlu)) return 0;
+  if (m.cfg.dtype == WD_DTYPE_BF16 && !m.cfg.weight_fp8) {
+    const wd::GemmPlan gp = wd::plan_gemm_bf16(M, 2 * F, H);
+    if (gp.dma_mfw && gp.splits == 1) return 1;
+  }
+  return 2;
+}
+
+// Most floats of split-K partials one pass of the layer stack over M rows
+// writes (O and down always write them; Q/K/V and gate/up unless fused).
+size_t step_partial_floats(const wd_model& m, int M) {
+  const wd_model_config& c = m.cfg;
+  const int H = c.hidden, Q = c.n_heads * c.head_dim, F = c.ffn;
+  auto part = [&](int N, int K) { return (size_t)gemm_splits(c, M, N, K) * M * N; };
+  size_t v = std::max(part(H, Q), part(H, F));
+  if (!qkv_fused(m, M)) v = std::max(v, part(m.qkv_n, H));
+  if (gateup_path(m, M) == 2) v = std::max(v, part(2 * F, H));
+  return v;
+}
+
 template <typename T>
 wd_status run_layers(wd_seq* s, const Rows& r) {
   const wd_model& m = *s->m;
@@ -905,7 +973,7 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
     const LayerW& w = m.layers[l];
     T* kc = (T*)s->kc + (size_t)l * KVd * s->T;
     T* vc = (T*)s->vc + (size_t)l * KVd * s->T;
-    if (fused_rows(m, M, m.qkv_n, H, wd::kEpiQkv)) {
+    if (qkv_fused(m, M)) {
       hipEvent_t e0, e1;
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_qkv_fused((const uint16_t*)a, H, w.wqkv, M, m.qkv_n, H,
@@ -933,15 +1001,16 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
     }
     WD_TRY(gemm<T>(s, o, Q, w.wo, w.so, s->C, M, H, Q, 1 << 20, &S));
     WD_HIP(wd::residual_norm<T>(s->h, s->C, S, M, H, (const T*)w.ffn_norm, c.rms_eps, a, nullptr, st));
-    if (fused_rows(m, M, 2 * F, H, wd::kEpiSwiGlu)) {
+    const int gu = gateup_path(m, M);
+    if (gu == 0) {
       hipEvent_t e0, e1;
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_swiglu_fused((const uint16_t*)a, H, w.wgu, M, F, H, (uint16_t*)sw, st,
                                         e0, e1, w.sgu));
       WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, 2 * F, H, m.esz, (double)M * F * m.esz));
-    } else if (const wd::GemmPlan gp = wd::plan_gemm_bf16(M, 2 * F, H);
-               c.dtype == WD_DTYPE_BF16 && !w.sgu && gp.dma_mfw && gp.splits == 1) {
+    } else if (gu == 1) {
       // many rows without a K split: SwiGLU in the GEMM's epilogue
+      const wd::GemmPlan gp = wd::plan_gemm_bf16(M, 2 * F, H);
       hipEvent_t e0, e1;
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_swiglu_dma((const uint16_t*)a, H, w.wgu, (uint16_t*)sw, M, F, H, gp, st,
@@ -1413,6 +1482,63 @@ wd_status wd_step(wd_seq* s, wd_step_out* out) {
   s->t++;
   if (out) return fetch_out(s, out, step, refresh ? 1 : 0, rows, nsel);
   return WD_OK;
+}
+
+wd_status wd_step_noalloc(wd_seq* s, wd_step_out* out) {
+  if (!s) return fail(WD_ERR_INVALID_ARG, "seq is NULL");
+  wd_model& m = *s->m;
+  const wd_model_config& c = m.cfg;
+  if (s->eos_id >= 0)
+    return fail(WD_ERR_UNSUPPORTED, "wd_step_noalloc does not take adaptive termination (use wd_step)");
+  if (m.profile)
+    return fail(WD_ERR_UNSUPPORTED, "kernel timing creates HIP events; disable it for wd_step_noalloc");
+  if (s->mode == 2) return fail(WD_ERR_STATE, "sequence is driven by wd_full_step");
+  if (s->cnt.u == 0) return fail(WD_ERR_STATE, "every position is decoded");
+  void* base = m.device >= 0 && m.device < kMaxDevices ? g_scratch_dev[m.device] : nullptr;
+  if (!base) return fail(WD_ERR_DEVICE, "no static scratch address for device %d", m.device);
+  // the rows this step runs through the layer stack and the LM head, counted
+  // as wd_step will count them (on a copy of the schedule's counts)
+  Counts cn = s->cnt;
+  const bool due = cn.phase_due();
+  if (due) cn.start_phase();
+  int rows = 0;
+  if (cn.j == 0) {
+    for (int b = 0; b < s->B; ++b)
+      rows += cn.refresh_rows(due ? cn.ctx(s->S[b]) : s->ctx[b], s->win.buffer_refresh);
+  } else {
+    rows = s->B * (cn.n_active() + cn.dp);
+  }
+  const int n_act_rows = s->B * cn.n_active();
+  const size_t part_bytes = step_partial_floats(m, rows) * 4;
+  const size_t attn_bytes =
+      c.dtype == WD_DTYPE_BF16
+          ? (size_t)std::min<long>(s->attn_part_floats,
+                                   8L * rows * c.n_heads * (c.head_dim + 2)) * 4
+          : 0;
+  const size_t conf_bytes =
+      (size_t)3 * n_act_rows * std::max<long>(wd::kConfChunks, c.vocab / 64) * 4;
+  const size_t need = align256(part_bytes) + align256(attn_bytes) + align256(conf_bytes);
+  if (need > kStaticScratchBytes)
+    return fail(WD_ERR_OUT_OF_MEMORY,
+                "step %d runs %d rows and needs %zu bytes of scratch; the static scratch holds %zu "
+                "(use wd_step)", s->t, rows, need, kStaticScratchBytes);
+  // the same step with its scratch redirected: plans and sizes are unchanged
+  // (the capacities the kernels are told stay the workspace's; what they
+  // touch fits in the regions above)
+  struct Restore {
+    wd_seq* s;
+    float *part, *attn, *conf;
+    ~Restore() {
+      s->C = part;
+      s->attn_part = attn;
+      s->conf_scratch = conf;
+    }
+  } restore{s, s->C, s->attn_part, s->conf_scratch};
+  char* p = (char*)base;
+  s->C = (float*)p;
+  s->attn_part = (float*)(p + align256(part_bytes));
+  s->conf_scratch = (float*)(p + align256(part_bytes) + align256(attn_bytes));
+  return wd_step(s, out);
 }
 
 wd_status wd_full_step(wd_seq* s, wd_step_out* out) {
