@@ -50,7 +50,7 @@ def log(msg):
 # source file that holds it (its hash gates the stored counter traffic)
 KERNEL_CLASSES = {1: "k_gemm_bf16", 2: "k_gemm_bf16_dma", 4: "k_attn_bf16"}
 PROFILE_NAMES = KERNEL_CLASSES
-KERNEL_SOURCES = {"k_gemm_bf16": "gemm.hip", "k_gemm_bf16_dma": "gemm.hip",
+KERNEL_SOURCES = {"k_gemm_bf16": "gemm.hip", "k_gemm_bf16_dma": "gemm_tiles.hip",
                   "k_attn_bf16": "layer.hip"}
 
 

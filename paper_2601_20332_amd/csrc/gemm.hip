@@ -985,207 +985,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
 // full-sequence path, batches): 128-row tiles, 2 weight groups per wave,
 // software-pipelined, K splits until 256 workgroups run (split-K partials
 // cost rows*N*4 bytes each).
-// ---- bf16 GEMM for many rows: multi-stage LDS pipeline fed by direct-to-LDS loads -------
-// Workgroup tile: 64 * MFW rows x 32 * TNB features (256, 192 or 128); wave
-// (wm, wn) computes 32 * MFW rows x 32 * TNB / (NW / 2) features (256: 128
-// with 4 waves, 64 with 8; 192: 32 with 12; 128: 32 with 8) on
-// v_mfma_f32_32x32x16_bf16 (weights as the A operand, activations as B).
-// Each 32-wide K step
-// is one stage in LDS, filled by 16-byte direct-to-LDS loads (lane l of a
-// load lands at +16 l) ST - 1 stages ahead of the step being computed; one
-// barrier per stage, with the waits issued by hand so that the compiler does
-// not drain every load at the barrier.
-// Stage layout (1 KB blocks after a 1 KB pad that keeps every load target off
-// LDS address 0):
-//   activation blocks 0 .. 4 MFW - 1: tile rows 16 b .. 16 b + 15, 64 bytes
-//     each; the 16-byte chunk c of row r sits in slot c ^ swz(r), with
-//     swz(r) = ((r >> 1) ^ (r >> 2)) & 3, so the 32-row operand reads hit
-//     distinct banks;
-//   weight blocks 4 MFW + 2 i + h: the A operand of feature block i (packed
-//     groups 2 i, 2 i + 1 of the tile) for K half h, assembled by the loads
-//     themselves from the two packed 16x32 fragments: rows of 16 lanes
-//     [g0 h0 g1 h1] (h = 0) and [g2 h2 g3 h3] (h = 1).
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-// at most N vector-memory operations of this wave outstanding (vmcnt in bits
-// 3:0 and 15:14; expcnt and lgkmcnt left unconstrained)
-#define WD_WAIT_VM(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | 0x70 | 0xF00 | ((((N) >> 4) & 3) << 14))
-// every LDS operation of this wave complete (lgkmcnt 0; vmcnt, expcnt free)
-#define WD_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xC07F)
 
-// SWIGLU (no K split, weights packed kPackGateUp): lane values of packed
-// groups 2 i + h come as gate (e / 4 = 2 h) and up (e / 4 = 2 h + 1) of the
-// same features, so the epilogue writes out[m][f] = silu(gate) * up (bf16,
-// F = N / 2 per row) instead of the fp32 products.
-// TNB: 32-feature blocks per tile (8: 256 features, 6: 192, 4: 128).  NW: waves per
-// workgroup, in two row halves; the NW / 2 waves of a half split the TNB
-// blocks evenly (8 waves and 256 features: two waves per SIMD, 64 features
-// each).
-template <int MFW, int ST, bool SWIGLU = false, int NW = 4, int TNB = 8>
-__global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __restrict__ X, int ldx,
-                                                          const u32x4* __restrict__ Wp,
-                                                          float* __restrict__ C, int M, int N,
-                                                          int K, int NB, int MT, int S, int ks,
-                                                          uint16_t* __restrict__ out) {
-  // the host pass only needs the kernel's signature
-#if defined(__HIP_DEVICE_COMPILE__)
-  static_assert(NW % 2 == 0 && TNB % (NW / 2) == 0, "waves split the feature blocks evenly");
-  constexpr int NFW = TNB / (NW / 2);    // 32-feature blocks of each wave
-  constexpr int F = 4 * MFW + 2 * TNB;   // 1 KB blocks per stage
-  constexpr int FW = (F + NW - 1) / NW;  // blocks wave w loads: w, w + NW, ... below F
-  constexpr int FWMIN = F / NW;          // blocks every wave loads
-  constexpr int STAGE16 = (F + 1) * 64;  // u32x4 per stage buffer, pad included
-  static_assert(ST >= 3 && ST <= 4, "stages");
-  static_assert((ST - 2) * FW < 64, "outstanding loads fit the wait counter");
-  __shared__ __attribute__((aligned(16))) u32x4 st0[STAGE16], st1[STAGE16], st2[STAGE16],
-      st3[ST > 3 ? STAGE16 : 1];
-  const int G = NB * MT * S;
-  int id = blockIdx.x;
-  if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);
-  const int mt = id % MT, rest = id / MT, nb = rest % NB, sp = rest / NB;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wm = wave & 1, wn = wave >> 1;
-  const int KT = K >> 5;
-  const int kt0 = sp * ks, nkt = min(KT, kt0 + ks) - kt0;
-  const int m0 = mt * 64 * MFW;
-  // per-lane source of every block this wave loads, at K step kt0
-  const u32x4* src[FW];
-  int step16[FW];  // u32x4 between consecutive K steps
-#pragma unroll
-  for (int q = 0; q < FW; ++q) {
-    const int f = min(wave + NW * q, F - 1);  // a wave past F never issues this slot
-    if (f < 4 * MFW) {
-      const int r = f * 16 + (lane >> 2);
-      const int c = (lane & 3) ^ (((r >> 1) ^ (r >> 2)) & 3);
-      const long row = min(m0 + r, M - 1);
-      src[q] = (const u32x4*)(X + row * ldx + kt0 * 32 + c * 8);
-      step16[q] = 4;
-    } else {
-      const int i = (f - 4 * MFW) >> 1, h = f & 1;
-      const int g = 2 * (nb * TNB + i) + ((lane >> 4) & 1);
-      const int sl = (lane & 15) + 16 * (2 * h + (lane >> 5));
-      src[q] = Wp + ((long)g * KT + kt0) * 64 + sl;
-      step16[q] = 64;
-    }
-  }
-  auto stage = [&](auto B) -> u32x4* {
-    constexpr int b = decltype(B)::value;
-    if constexpr (b == 0) return st0 + 64;
-    else if constexpr (b == 1) return st1 + 64;
-    else if constexpr (b == 2) return st2 + 64;
-    else return st3 + 64;
-  };
-  auto issue = [&](auto B, int it) {
-    const int k = min(it, nkt - 1);  // steps past the split reload its last one, unused
-    u32x4* dst = stage(B);
-#pragma unroll
-    for (int q = 0; q < FW; ++q)
-      if (q < FWMIN || wave + NW * q < F)  // uniform over the wave
-        __builtin_amdgcn_global_load_lds(src[q] + (long)k * step16[q], dst + (wave + NW * q) * 64,
-                                         16, 0, 0);
-  };
-  f32x16 acc[NFW][MFW];
-#pragma unroll
-  for (int a = 0; a < NFW; ++a)
-#pragma unroll
-    for (int b = 0; b < MFW; ++b)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
-  // Per-lane offsets (u32x4) of this wave's operands inside a stage: weight
-  // block 4 MFW + 2 (wn NFW + ii) + h, and activation row (wm MFW + jj) 32 +
-  // l % 32 in slot (2 h + l / 32) ^ swz(l) (swz only sees the row's low bits).
-  // They are kept opaque so that each operand read is its stage buffer plus
-  // one offset and a constant: the LDS lowering tags an access with its buffer
-  // only a few address steps deep, and for an untagged read the compiler
-  // waits for every direct-to-LDS load in flight.
-  int a_off = (4 * MFW + 2 * wn * NFW) * 64 + lane;
-  int x_off0 = wm * MFW * 128 + (lane & 31) * 4 + (((lane >> 5) ^ (lane >> 1) ^ (lane >> 2)) & 3);
-  int x_off1 = wm * MFW * 128 + (lane & 31) * 4 + ((2 + (lane >> 5)) ^ (((lane >> 1) ^ (lane >> 2)) & 3));
-  asm volatile("" : "+v"(a_off), "+v"(x_off0), "+v"(x_off1));
-  auto compute = [&](auto B) {
-    const u32x4* sb = stage(B);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      u32x4 a[NFW], bx[MFW];
-#pragma unroll
-      for (int ii = 0; ii < NFW; ++ii) a[ii] = sb[a_off + ii * 128 + h * 64];
-#pragma unroll
-      for (int jj = 0; jj < MFW; ++jj) bx[jj] = sb[(h ? x_off1 : x_off0) + jj * 128];
-#pragma unroll
-      for (int jj = 0; jj < MFW; ++jj)
-#pragma unroll
-        for (int ii = 0; ii < NFW; ++ii) acc[ii][jj] = mfma32(a[ii], bx[jj], acc[ii][jj]);
-    }
-  };
-  // step it: its loads are done (this wave: at most the later stages' loads
-  // outstanding; every wave: the barrier), every wave has finished reading the
-  // buffer of step it - 1, which is refilled with step it + ST - 1
-  auto body = [&](auto J, int it) {
-    constexpr int j = decltype(J)::value;
-    // a wave that loads more than FWMIN blocks per stage waits for more than it must
-    WD_WAIT_VM((ST - 2) * FWMIN);
-    WD_WAIT_LGKM0();
-    __builtin_amdgcn_s_barrier();
-    issue(ic<(j + ST - 1) % ST>{}, it + ST - 1);
-    if (it < nkt) compute(ic<j % ST>{});
-  };
-  issue(ic<0>{}, 0);
-  issue(ic<1>{}, 1);
-  if constexpr (ST > 3) issue(ic<2>{}, 2);
-  for (int it = 0; it < nkt; it += ST) {
-    body(ic<0>{}, it);
-    body(ic<1>{}, it + 1);
-    body(ic<2>{}, it + 2);
-    if constexpr (ST > 3) body(ic<3>{}, it + 3);
-  }
-  WD_WAIT_VM(0);  // no load may land in LDS after the workgroup ends
-  // D of (feature block i, row block j): lane l holds row j * 32 + l % 32,
-  // features i * 32 + (e / 4) * 8 + (l / 32) * 4 + e % 4
-#pragma unroll
-  for (int ii = 0; ii < NFW; ++ii)
-#pragma unroll
-    for (int jj = 0; jj < MFW; ++jj) {
-      const int m = m0 + (wm * MFW + jj) * 32 + (lane & 31);
-      if (m >= M) continue;
-      if constexpr (SWIGLU) {
-        const int F = N >> 1;
-        const int i = nb * TNB + wn * NFW + ii;
-#pragma unroll
-        for (int hg = 0; hg < 2; ++hg) {
-          const int f0 = (2 * i + hg) * 8 + (lane >> 5) * 4;
-          float y[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float x = acc[ii][jj][8 * hg + j], u = acc[ii][jj][8 * hg + 4 + j];
-            y[j] = x / (1.0f + expf(-x)) * u;
-          }
-          u32x2 w;
-          w.x = (uint32_t)f2bf(y[0]) | ((uint32_t)f2bf(y[1]) << 16);
-          w.y = (uint32_t)f2bf(y[2]) | ((uint32_t)f2bf(y[3]) << 16);
-          *(u32x2*)(out + (long)m * F + f0) = w;
-        }
-        continue;
-      }
-      const int n0 = (nb * TNB + wn * NFW + ii) * 32 + (lane >> 5) * 4;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 v = {acc[ii][jj][g * 4], acc[ii][jj][g * 4 + 1], acc[ii][jj][g * 4 + 2],
-                         acc[ii][jj][g * 4 + 3]};
-        *(f32x4*)(C + ((long)sp * M + m) * N + n0 + g * 8) = v;
-      }
-    }
-#endif
-}
-
-// Waves of the many-row kernel: with 256-feature tiles 8 (two per SIMD, 64
-// features each) measured 2-8% faster than 4 on the refresh shapes (224-384
-// rows, weights from HBM): Q/K/V at 384 rows 51.7 us against 54.8, gate/up
-// 91.9 against 94.1, down 47.0 against 50.7.  With 192-feature tiles 12 (three
-// per SIMD, 32 features each) beat 6 by up to 10%.
-constexpr int kDmaWaves = 8, kDmaWaves192 = 12;
 
 GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
   GemmPlan p;
@@ -1289,6 +1089,15 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
     p.splits = pick->splits;
     p.ks_per_split = pick->ks;
     p.grid = (int)pick->grid;
+    p.dma_nw = pick->tnb == 6 ? 12 : 8;
+    p.dma_gm = 0;
+    if (p.grid > 512 && pick->mfw == 4 && pick->tnb == 8) {
+      // several rounds of 256 x 256 tiles (batches, long full-sequence
+      // steps): one wave per SIMD with the pinned schedule, in bands of 8
+      // row tiles (measured at 12000 rows; gemm_tiles.hip)
+      p.dma_nw = 4;
+      p.dma_gm = 8;
+    }
     p.mf = 8;
     p.nf = 4;
     p.ck = 1;
@@ -1334,39 +1143,6 @@ static void launch_mf(dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, c
   }
 }
 
-// the k_gemm_bf16_dma instance of plan p (tile rows, tile width, waves);
-// false if the plan names none
-template <bool SWIGLU, typename... A>
-static bool launch_dma(const GemmPlan& p, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
-                       A... args) {
-  const dim3 b8(64 * kDmaWaves), b6(64 * kDmaWaves192);
-  if (p.dma_tnb == 8) {
-    switch (p.dma_mfw) {
-      case 4: launch_timed_block(k_gemm_bf16_dma<4, 3, SWIGLU, kDmaWaves, 8>, grid, b8, st, e0, e1, args...); return true;
-      case 3: launch_timed_block(k_gemm_bf16_dma<3, 4, SWIGLU, kDmaWaves, 8>, grid, b8, st, e0, e1, args...); return true;
-      case 2: launch_timed_block(k_gemm_bf16_dma<2, 4, SWIGLU, kDmaWaves, 8>, grid, b8, st, e0, e1, args...); return true;
-      default: return false;
-    }
-  }
-  if (p.dma_tnb == 6) {
-    switch (p.dma_mfw) {
-      case 4: launch_timed_block(k_gemm_bf16_dma<4, 3, SWIGLU, kDmaWaves192, 6>, grid, b6, st, e0, e1, args...); return true;
-      case 3: launch_timed_block(k_gemm_bf16_dma<3, 4, SWIGLU, kDmaWaves192, 6>, grid, b6, st, e0, e1, args...); return true;
-      case 2: launch_timed_block(k_gemm_bf16_dma<2, 4, SWIGLU, kDmaWaves192, 6>, grid, b6, st, e0, e1, args...); return true;
-      default: return false;
-    }
-  }
-  if (p.dma_tnb == 4) {
-    switch (p.dma_mfw) {
-      case 4: launch_timed_block(k_gemm_bf16_dma<4, 3, SWIGLU, kDmaWaves, 4>, grid, b8, st, e0, e1, args...); return true;
-      case 3: launch_timed_block(k_gemm_bf16_dma<3, 4, SWIGLU, kDmaWaves, 4>, grid, b8, st, e0, e1, args...); return true;
-      case 2: launch_timed_block(k_gemm_bf16_dma<2, 4, SWIGLU, kDmaWaves, 4>, grid, b8, st, e0, e1, args...); return true;
-      default: return false;
-    }
-  }
-  return false;
-}
-
 bool gemm_plan_ok(const GemmPlan& p, int M, int N, int K, bool w8, bool swiglu) {
   if (M <= 0 || N <= 0 || K <= 0 || K % 32) return false;
   const int KT = K / 32;
@@ -1384,6 +1160,12 @@ bool gemm_plan_ok(const GemmPlan& p, int M, int N, int K, bool w8, bool swiglu) 
     if (w8 || p.dma_mfw < 2 || p.dma_mfw > 4 ||
         (p.dma_tnb != 8 && p.dma_tnb != 6 && p.dma_tnb != 4) || N % TN)
       return false;
+    // the instances the launcher has: 12 waves with 192-feature tiles, 8
+    // with the others, 4 only with 256 x 256 tiles; bands of 0 or 8 row tiles
+    const bool waves_ok = p.dma_tnb == 6 ? p.dma_nw == 12
+                                         : p.dma_nw == 8 || (p.dma_nw == 4 && p.dma_tnb == 8 &&
+                                                             p.dma_mfw == 4);
+    if (!waves_ok || (p.dma_gm != 0 && p.dma_gm != 8)) return false;
     const long MT = (M + 64L * p.dma_mfw - 1) / (64L * p.dma_mfw);
     return (long)(N / TN) * MT * p.splits == p.grid && (!swiglu || p.splits == 1);
   }
@@ -1405,7 +1187,7 @@ void gemm_plan_tile(const GemmPlan& p, int* kernel, int* rows, int* features, in
     *kernel = 2;
     *rows = 64 * p.dma_mfw;
     *features = 32 * p.dma_tnb;
-    *waves = p.dma_tnb == 6 ? kDmaWaves192 : kDmaWaves;
+    *waves = p.dma_nw;
   } else {
     *kernel = 3;
     *rows = 16 * p.mf;
@@ -1424,10 +1206,7 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
                                  ev_start, ev_stop, wsc);
   }
   if (p.dma_mfw) {
-    const int TN = 32 * p.dma_tnb;
-    const int NB = N / TN, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
-    if (!launch_dma<false>(p, dim3(p.grid), st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp, C, M,
-                           N, K, NB, MT, p.splits, p.ks_per_split, (uint16_t*)nullptr))
+    if (!launch_gemm_tiles(p, X, ldx, Wp, C, M, N, K, nullptr, st, ev_start, ev_stop))
       return hipErrorInvalidValue;
     return hipGetLastError();
   }
@@ -1459,10 +1238,7 @@ hipError_t gemm_bf16_swiglu_dma(const uint16_t* X, int ldx, const void* Wp, uint
   const int N = 2 * F;
   if (M <= 0) return hipSuccess;
   if (!p.dma_mfw || !gemm_plan_ok(p, M, N, K, false, true)) return hipErrorInvalidValue;
-  const int KT = K / 32, NB = N / (32 * p.dma_tnb);
-  const int MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
-  if (!launch_dma<true>(p, dim3(p.grid), st, ev_start, ev_stop, X, ldx, (const u32x4*)Wp,
-                        (float*)nullptr, M, N, K, NB, MT, 1, KT, out))
+  if (!launch_gemm_tiles(p, X, ldx, Wp, nullptr, M, N, K, out, st, ev_start, ev_stop))
     return hipErrorInvalidValue;
   return hipGetLastError();
 }

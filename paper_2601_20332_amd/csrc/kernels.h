@@ -21,6 +21,9 @@ struct GemmPlan {
   int grid = 0;
   int dma_mfw = 0;       // > 0: k_gemm_bf16_dma with 64 * dma_mfw-row tiles
   int dma_tnb = 8;       // its 32-feature blocks per tile: 8, 6 or 4 (256, 192, 128 features)
+  int dma_nw = 0;        // its waves per workgroup: 12 (192 features), 8, or 4 (256 x 256 tiles,
+                         // operand reads pinned ahead of the MFMAs)
+  int dma_gm = 0;        // > 0: its workgroups in bands of dma_gm row tiles
   int fused_gw = 0;      // > 0: gemm_bf16_split_fused with fused_gw groups per workgroup
 };
 // Launch plan for C = X W^T; at most max_splits K splits.
@@ -30,6 +33,12 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8 = false, int max_splits = 1
 // workgroup).  gemm_bf16 and gemm_bf16_swiglu_dma reject plans for which
 // this is false.
 bool gemm_plan_ok(const GemmPlan& p, int M, int N, int K, bool w8, bool swiglu);
+// The many-row kernel (gemm_tiles.hip) for plan p (p.dma_mfw > 0, checked by
+// gemm_plan_ok): split-K partials into C, or with swiglu_out the SwiGLU
+// epilogue (no K split).  False if the plan names no instance.
+bool launch_gemm_tiles(const GemmPlan& p, const uint16_t* X, int ldx, const void* Wp, float* C,
+                       int M, int N, int K, uint16_t* swiglu_out, hipStream_t st, hipEvent_t e0,
+                       hipEvent_t e1);
 // The kernel plan p launches (1 pipelined few-row kernel with K-split
 // partials, 2 the many-row LDS-pipelined kernel, 3 the split-K tiled kernel)
 // and its workgroup tile and waves.

@@ -41,7 +41,10 @@ def _check(M, N, K, fp8, max_splits=1 << 20):
         assert M <= 96 and p["rows"] >= M and p["waves"] in (2, 3, 4, 6, 7), where
     elif p["kernel"] == 2:  # many-row kernel: bf16 weights only
         assert not fp8 and M > 64 and p["features"] in (256, 192, 128), where
-        assert p["waves"] == (12 if p["features"] == 192 else 8), where
+        if p["waves"] == 4:  # several rounds of 256 x 256 tiles: one wave per SIMD
+            assert (p["rows"], p["features"]) == (256, 256) and p["workgroups"] > 512, where
+        else:
+            assert p["waves"] == (12 if p["features"] == 192 else 8), where
         if p["features"] < 256:  # narrower tiles only within two rounds
             assert p["workgroups"] <= 512, where
         # the step loop applies SwiGLU in this kernel whenever K is not split
