@@ -474,6 +474,196 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
   }
 }
 
+// Grouped K/V heads (n_kv < n_heads) with many rows per sequence (refresh
+// steps): the same computation with one workgroup per (K/V head, block of
+// 16 NWQ columns), a column being a (query head of the group, row) pair, so
+// that every K/V tile a workgroup stages serves all the query heads that
+// read it.  The first 256 threads stage the tiles as above.  Measured at the
+// Dream-7B shape (28 query / 4 K/V heads), isolated: 600 rows x 600 keys
+// 40.5 us (8 waves, no key split) against 51.5 us per query head; at
+// normal-step shapes (34-46 rows x 416-768 keys, 0.85-1.6 MB of K/V per
+// layer) grouping does not pay (0.95-1.01x at every split count tried): the
+// kernel is bound by the latency of its few tile steps there, not by loads.
+template <int NWQ>
+__global__ __launch_bounds__(64 * NWQ) void k_attn_bf16_grouped(const uint16_t* __restrict__ q,
+                                                   const uint16_t* __restrict__ kc,
+                                                   const uint16_t* __restrict__ vc,
+                                                   long cache_rows, uint16_t* __restrict__ o,
+                                                   WdStepGeom g, int nh, int nkv, int nsplit,
+                                                   int keys_per_split, int M,
+                                                   float* __restrict__ part,
+                                                   float* __restrict__ ml) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKT * kKPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[kAttD * kVPitch];
+  // blockIdx.x = K/V head; the columns of a workgroup are (query head of the
+  // group, row) pairs, head-major: column i is head kvh * G + i / nq, row i % nq
+  const int kvh = blockIdx.x, b = blockIdx.y;
+  const int qb = blockIdx.z / nsplit, split = blockIdx.z % nsplit;
+  const int nq = g.nrows[b];
+  const int G = nh / nkv, ncol = G * nq;
+  constexpr int QB = 16 * NWQ;
+  if (qb * QB >= ncol) return;
+  const int key_lo = split * keys_per_split;
+  const int c = min(g.ctx[b], key_lo + keys_per_split);
+  const long off = g.off[b];
+  const int row0 = g.row0[b];
+  const uint16_t* kb = kc + ((long)kvh * cache_rows + off) * kAttD;
+  const uint16_t* vb = vc + ((long)kvh * cache_rows + off) * kAttD;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int col = qb * QB + wave * 16 + l16;  // this lane's column of S^T / O^T
+  const bool qvalid = col < ncol;
+  const int h = kvh * G + (qvalid ? col / nq : 0), qi = qvalid ? col % nq : 0;
+  const bool wave_active = qb * QB + wave * 16 < ncol;
+  const bool loader = tid < 256;  // the first 256 threads stage the K/V tiles
+  const long ldq = (long)nh * kAttD;
+
+  u32x4 qf[4];
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int cc = 0; cc < 4; ++cc)
+    qf[cc] = qvalid ? *(const u32x4*)(q + (long)(row0 + qi) * ldq + h * kAttD + cc * 32 + grp * 8)
+                    : zero4;
+
+  f32x4 oacc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) oacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float scale = 0.08838834764831845f;  // 1/sqrt(128)
+
+  // K/V tile of 64 keys x 256 B each: thread tid covers keys (tid >> 4) + 16 i,
+  // 16-byte chunk tid & 15 (dims 8 (tid & 15) ..).  The next tile's loads are
+  // issued before the current tile is computed; addresses are clamped to the
+  // last key and the keys past c are zeroed when the tile is stored.
+  const int tkey = tid >> 4, tch = tid & 15;
+  u32x4 kr[4], vr[4];
+  auto load_tile = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const long kk = min(j0 + tkey + 16 * i, c - 1);
+      kr[i] = *(const u32x4*)(kb + kk * kAttD + tch * 8);
+      vr[i] = *(const u32x4*)(vb + kk * kAttD + tch * 8);
+    }
+  };
+  if (loader && key_lo < c) load_tile(key_lo);
+  for (int j0 = key_lo; j0 < c; j0 += kKT) {
+    __syncthreads();
+    if (loader) {
+    // K rows at the score row that holds them; V^T dims as 4-key runs
+    u32x4 vv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = tkey + 16 * i;  // k16 = tkey, kq = i
+      const bool ok = j0 + key < c;
+      const u32x4 kv = ok ? kr[i] : zero4;
+      vv[i] = ok ? vr[i] : zero4;
+      const int st = 2 * (tkey >> 3) + (tkey & 1), r = 4 * ((tkey >> 1) & 3) + i;
+      *(u32x4*)(Ks + (st * 16 + r) * kKPitch + tch * 8) = kv;
+    }
+    {
+      const int chunk = (tkey >> 1) ^ (tch & 7);  // dims tch * 8 .. have d / 8 = tch
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int sh = 16 * (e & 1);
+        u32x2 w;
+        w.x = ((vv[0][e >> 1] >> sh) & 0xffffu) | (((vv[1][e >> 1] >> sh) & 0xffffu) << 16);
+        w.y = ((vv[2][e >> 1] >> sh) & 0xffffu) | (((vv[3][e >> 1] >> sh) & 0xffffu) << 16);
+        *(u32x2*)(Vt + (tch * 8 + e) * kVPitch + chunk * 8 + (tkey & 1) * 4) = w;
+      }
+    }
+    }
+    __syncthreads();
+    if (loader) load_tile(min(j0 + kKT, c - 1));
+    if (!wave_active) continue;
+
+    // S^T[key][query] for 4 subtiles of 16 keys
+    f32x4 sacc[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      sacc[st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const u32x4 ka = *(const u32x4*)(Ks + (st * 16 + l16) * kKPitch + cc * 32 + grp * 8);
+        sacc[st] = mfma16(ka, qf[cc], sacc[st]);
+      }
+    }
+    // this lane holds keys pi(st, grp * 4 + jj) for query l16
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int key = j0 + 16 * jj + 8 * (st >> 1) + 2 * grp + (st & 1);
+        const float s = key < c ? sacc[st][jj] * scale : -INFINITY;
+        sacc[st][jj] = s;
+        tmax = fmaxf(tmax, s);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float m_new = fmaxf(m_run, tmax);
+    const float corr = expf(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const float pv = expf(sacc[st][jj] - m_new);
+        sacc[st][jj] = pv;
+        psum += pv;
+      }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * corr + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) oacc[i] *= corr;
+
+    // O^T += V^T P^T over two 32-position chunks (subtiles 2pc, 2pc+1)
+#pragma unroll
+    for (int pc = 0; pc < 2; ++pc) {
+      // element e of lane grp's fragment is V^T position 32 pc + 8 grp + e, the key
+      // of score subtile 2 pc + e / 4, row grp * 4 + e % 4
+      u32x4 bhi, blo;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4& sp = sacc[2 * pc + (i >> 1)];
+        const float p0 = sp[(2 * i) & 3], p1 = sp[(2 * i + 1) & 3];
+        const uint16_t h0 = f2bf(p0), h1 = f2bf(p1);
+        bhi[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        blo[i] = (uint32_t)f2bf(p0 - bf2f(h0)) | ((uint32_t)f2bf(p1 - bf2f(h1)) << 16);
+      }
+#pragma unroll
+      for (int df = 0; df < 8; ++df) {
+        const int d = df * 16 + l16;
+        const u32x4 va = *(const u32x4*)(Vt + d * kVPitch + (((4 * pc + grp) ^ ((d >> 3) & 7)) * 8));
+        oacc[df] = mfma16(va, bhi, oacc[df]);
+        oacc[df] = mfma16(va, blo, oacc[df]);
+      }
+    }
+  }
+  if (!qvalid) return;
+  if (nsplit > 1) {
+    const long pr = ((long)split * M + row0 + qi) * nh + h;
+    float* prow = part + pr * kAttD;
+#pragma unroll
+    for (int df = 0; df < 8; ++df) *(f32x4*)(prow + df * 16 + grp * 4) = oacc[df];
+    if (grp == 0) {
+      ml[pr * 2] = m_run;
+      ml[pr * 2 + 1] = l_run;
+    }
+    return;
+  }
+  const float inv = 1.0f / l_run;
+  uint16_t* orow = o + (long)(row0 + qi) * ldq + h * kAttD;
+#pragma unroll
+  for (int df = 0; df < 8; ++df) {
+    u32x2 w;
+    w.x = (uint32_t)f2bf(oacc[df][0] * inv) | ((uint32_t)f2bf(oacc[df][1] * inv) << 16);
+    w.y = (uint32_t)f2bf(oacc[df][2] * inv) | ((uint32_t)f2bf(oacc[df][3] * inv) << 16);
+    *(u32x2*)(orow + df * 16 + grp * 4) = w;
+  }
+}
+
 // out = sum_s exp(m_s - m) O_s / sum_s exp(m_s - m) l_s, m = max_s m_s
 __global__ __launch_bounds__(128) void k_attn_combine(const float* __restrict__ part,
                                                       const float* __restrict__ ml, int nsplit,
@@ -522,12 +712,36 @@ hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint1
     qblocks += (g.nrows[b] + 63) / 64;
   }
   if (nqmax <= 0) return hipSuccess;
+  if (n_kv < n_heads && nqmax >= 256) {
+    // refresh-step rows with grouped K/V heads: each staged tile serves the
+    // group's query heads; no key split (so no merge)
+    constexpr int NWQ = 8;
+    const int G = n_heads / n_kv;
+    const int blocks = (G * nqmax + 16 * NWQ - 1) / (16 * NWQ);
+    const int tiles = (cmax + kKT - 1) / kKT;
+    dim3 grid(n_kv, g.batch, blocks);
+    if (e0)
+      hipExtLaunchKernelGGL(k_attn_bf16_grouped<NWQ>, grid, dim3(64 * NWQ), 0, st, e0, e1, 0, q,
+                            kcache, vcache, cache_rows, o, g, n_heads, n_kv, 1, tiles * kKT, M,
+                            part, part);
+    else
+      hipLaunchKernelGGL(k_attn_bf16_grouped<NWQ>, grid, dim3(64 * NWQ), 0, st, q, kcache, vcache,
+                         cache_rows, o, g, n_heads, n_kv, 1, tiles * kKT, M, part, part);
+    return hipGetLastError();
+  }
   // split the keys until about 512 workgroups run, into at most 8 splits, if
   // the partial buffer allows.  Measured (isolated, 32 heads): 16 one-tile
   // splits cost more than 8 two-tile ones (1024 keys: 20.8 against 17.4 us at
-  // 64 rows, 16.1 against 14.8 at 34), the combine reading every split.
+  // 64 rows, 16.1 against 14.8 at 34), the combine reading every split.  But
+  // once the unsplit grid has 128 workgroups (refresh-step rows), splitting
+  // costs more than it parallelizes: 32 heads, rows x keys 224 x 224 17.1 us
+  // unsplit against 21.7, 384 x 384 23.1 against 33.4, 832 x 832 55.4
+  // against 72.2 (2 splits).
   const int tiles = (cmax + kKT - 1) / kKT;
-  int nsplit = std::min<long>(tiles, std::max<long>(1, (512 + n_heads * qblocks - 1) / (n_heads * qblocks)));
+  int nsplit = n_heads * qblocks >= 128
+                   ? 1
+                   : std::min<long>(tiles, std::max<long>(1, (512 + n_heads * qblocks - 1) /
+                                                                 (n_heads * qblocks)));
   nsplit = std::min(nsplit, std::min(kMaxSplit, 8));
   while (nsplit > 1 && (long)nsplit * M * n_heads * (kAttD + 2) > part_floats) --nsplit;
   const int tps = (tiles + nsplit - 1) / nsplit;

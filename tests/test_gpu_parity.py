@@ -123,6 +123,15 @@ def test_bf16_edge_windows():
         _run_and_check(MICRO_MHA, prompts, 10, win)
 
 
+def test_bf16_gqa_refresh_rows_grouped_attention():
+    """Refresh steps of 300 and more rows with grouped K/V heads take the
+    attention kernel whose workgroups serve all query heads of a K/V head
+    (normal steps keep one workgroup per query head)."""
+    prompts = synth.prompts(MICRO_GQA, [300, 260])
+    steps, _, _ = _run_and_check(MICRO_GQA, prompts, 20, synth.WindowSettings(6, 10, 4, 2))
+    assert steps[0].res.is_refresh and steps[0].res.n_rows >= 2 * 256
+
+
 def test_bf16_pruning_only_every_step_refreshes():
     """Window pruning without the cache (the Table 1 setting of Sec. 5.2): R =
     1, so every step is a refresh over the retained prefix [0, c), with E = 8
