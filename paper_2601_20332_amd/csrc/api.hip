@@ -925,11 +925,17 @@ bool fused_rows(const wd_model& m, int M, int N, int K, int epi) {
 
 wd_model& m_mut(wd_seq* s) { return *s->m; }
 
-// Which kernels a layer's products take at M rows.  Q/K/V: the fused few-row
-// kernel writes q and the cache itself; otherwise split-K partials and
+// Which kernels a layer's products take at M rows.  Q/K/V: 0 = the fused
+// few-row kernel, 1 = the many-row kernel with the Q/K/V epilogue (no K
+// split); both write q and the cache themselves; 2 = split-K partials and
 // k_qkv_epilogue.
-bool qkv_fused(const wd_model& m, int M) {
-  return fused_rows(m, M, m.qkv_n, m.cfg.hidden, wd::kEpiQkv);
+int qkv_path(const wd_model& m, int M) {
+  if (fused_rows(m, M, m.qkv_n, m.cfg.hidden, wd::kEpiQkv)) return 0;
+  if (m.cfg.dtype == WD_DTYPE_BF16 && !m.cfg.weight_fp8) {
+    const wd::GemmPlan gp = wd::plan_gemm_bf16(M, m.qkv_n, m.cfg.hidden);
+    if (gp.dma_mfw && gp.splits == 1) return 1;
+  }
+  return 2;
 }
 // gate/up: 0 = the fused few-row kernel with SwiGLU, 1 = the many-row kernel
 // with SwiGLU in its epilogue (no K split), 2 = split-K partials and k_swiglu.
@@ -950,7 +956,7 @@ size_t step_partial_floats(const wd_model& m, int M) {
   const int H = c.hidden, Q = c.n_heads * c.head_dim, F = c.ffn;
   auto part = [&](int N, int K) { return (size_t)gemm_splits(c, M, N, K) * M * N; };
   size_t v = std::max(part(H, Q), part(H, F));
-  if (!qkv_fused(m, M)) v = std::max(v, part(m.qkv_n, H));
+  if (qkv_path(m, M) == 2) v = std::max(v, part(m.qkv_n, H));
   if (gateup_path(m, M) == 2) v = std::max(v, part(2 * F, H));
   return v;
 }
@@ -973,7 +979,8 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
     const LayerW& w = m.layers[l];
     T* kc = (T*)s->kc + (size_t)l * KVd * s->T;
     T* vc = (T*)s->vc + (size_t)l * KVd * s->T;
-    if (qkv_fused(m, M)) {
+    const int qp = qkv_path(m, M);
+    if (qp == 0) {
       hipEvent_t e0, e1;
       WD_TRY(profile_begin(m_mut(s), &e0, &e1));
       WD_HIP(wd::gemm_bf16_qkv_fused((const uint16_t*)a, H, w.wqkv, M, m.qkv_n, H,
@@ -981,6 +988,19 @@ wd_status run_layers(wd_seq* s, const Rows& r) {
                                      c.n_heads, c.n_kv_heads, (uint16_t*)q, (uint16_t*)kc,
                                      (uint16_t*)vc, s->T, st, e0, e1, w.sqkv));
       WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_ROWS, M, m.qkv_n, H, m.esz,
+                         (double)M * m.qkv_n * m.esz));
+    } else if (qp == 1) {
+      // many rows without a K split: bias, RoPE and the q / K/V stores in the
+      // GEMM's epilogue
+      const wd::GemmPlan gp = wd::plan_gemm_bf16(M, m.qkv_n, H);
+      const wd::QkvOut qo{(const uint16_t*)w.bqkv, s->rope, s->row_pos, s->row_tok,
+                          (uint16_t*)q, (uint16_t*)kc, (uint16_t*)vc, s->T, c.n_heads,
+                          c.n_kv_heads};
+      hipEvent_t e0, e1;
+      WD_TRY(profile_begin(m_mut(s), &e0, &e1));
+      WD_HIP(wd::gemm_bf16_qkv_tiles((const uint16_t*)a, H, w.wqkv, M, m.qkv_n, H, gp, qo, st, e0,
+                                     e1));
+      WD_TRY(profile_end(m_mut(s), WD_PROF_GEMM_TILED, M, m.qkv_n, H, m.esz,
                          (double)M * m.qkv_n * m.esz));
     } else {
       WD_TRY(gemm<T>(s, a, H, w.wqkv, w.sqkv, s->C, M, m.qkv_n, H, 1 << 20, &S));

@@ -1232,6 +1232,18 @@ hipError_t gemm_bf16(const uint16_t* X, int ldx, const void* Wp, float* C, int M
   return hipGetLastError();
 }
 
+hipError_t gemm_bf16_qkv_tiles(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
+                               const GemmPlan& p, const QkvOut& qo, hipStream_t st, hipEvent_t e0,
+                               hipEvent_t e1) {
+  if (M <= 0) return hipSuccess;
+  if (!p.dma_mfw || p.splits != 1 || N != (qo.nh + 2 * qo.nkv) * 128 ||
+      !gemm_plan_ok(p, M, N, K, false, true))
+    return hipErrorInvalidValue;
+  if (!launch_gemm_tiles(p, X, ldx, Wp, nullptr, M, N, K, nullptr, st, e0, e1, &qo))
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t gemm_bf16_swiglu_dma(const uint16_t* X, int ldx, const void* Wp, uint16_t* out, int M,
                                 int F, int K, const GemmPlan& p, hipStream_t st,
                                 hipEvent_t ev_start, hipEvent_t ev_stop) {

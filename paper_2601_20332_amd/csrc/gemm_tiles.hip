@@ -62,22 +62,32 @@ __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
 // every LDS operation of this wave complete (lgkmcnt 0; vmcnt, expcnt free)
 #define WD_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xC07F)
 
-// SWIGLU (no K split, weights packed kPackGateUp): lane values of packed
-// groups 2 i + h come as gate (e / 4 = 2 h) and up (e / 4 = 2 h + 1) of the
-// same features, so the epilogue writes out[m][f] = silu(gate) * up (bf16,
-// F = N / 2 per row) instead of the fp32 products.
+// Epilogues (EPI; the last two need all of K in one workgroup, S = 1):
+//   kTileEpiPartial: fp32 split-K partials C[s][m][n].
+//   kTileEpiSwiGlu (weights packed kPackGateUp): lane values of packed groups
+//     2 i + h come as gate (e / 4 = 2 h) and up (e / 4 = 2 h + 1) of the same
+//     features, so the epilogue writes out[m][f] = silu(gate) * up (bf16, F =
+//     N / 2 per row) instead of the fp32 products.
+//   kTileEpiQkv (weights packed kPackRopePair, head_dim 128): likewise a lane
+//     holds four dims of a head (e / 4 = 2 h) and their rotation partners 64
+//     dims on (e / 4 = 2 h + 1), so it adds the bias, rotates q and k at the
+//     row's position and stores q, k and v as bf16 (q to its row, k and v to
+//     the row's K/V cache row), as k_qkv_epilogue does from the partials.
 // TNB: 32-feature blocks per tile (8: 256 features, 6: 192, 4: 128).  NW: waves per
 // workgroup, in two row halves; the NW / 2 waves of a half split the TNB
 // blocks evenly (8 waves and 256 features: two waves per SIMD, 64 features
 // each; 4 waves: one per SIMD, 128 x 128 each).  SCH 1: the operand reads of
 // a K step pinned ahead of its MFMAs (for one wave per SIMD).  gm > 0:
 // workgroups in bands of gm row tiles (for grids of several rounds).
-template <int MFW, int ST, bool SWIGLU, int NW, int TNB, int SCH>
+constexpr int kTileEpiPartial = 0, kTileEpiSwiGlu = 1, kTileEpiQkv = 2;
+
+template <int MFW, int ST, int EPI, int NW, int TNB, int SCH>
 __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __restrict__ X, int ldx,
                                                           const u32x4* __restrict__ Wp,
                                                           float* __restrict__ C, int M, int N,
                                                           int K, int NB, int MT, int S, int ks,
-                                                          int gm, uint16_t* __restrict__ out) {
+                                                          int gm, uint16_t* __restrict__ out,
+                                                          QkvOut qo) {
   // the host pass only needs the kernel's signature
 #if defined(__HIP_DEVICE_COMPILE__)
   static_assert(NW % 2 == 0 && TNB % (NW / 2) == 0, "waves split the feature blocks evenly");
@@ -245,7 +255,55 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __
     for (int jj = 0; jj < MFW; ++jj) {
       const int m = m0 + (wm * MFW + jj) * 32 + (lane & 31);
       if (m >= M) continue;
-      if constexpr (SWIGLU) {
+      if constexpr (EPI == kTileEpiQkv) {
+        const int i = nb * TNB + wn * NFW + ii;
+#pragma unroll
+        for (int hg = 0; hg < 2; ++hg) {
+          const int grp = 2 * i + hg, head = grp >> 3;
+          const int d0 = (grp & 7) * 8 + (lane >> 5) * 4;  // dims d0 .. d0 + 3, partners + 64
+          float x0[4], x1[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            x0[j] = acc[ii][jj][8 * hg + j];
+            x1[j] = acc[ii][jj][8 * hg + 4 + j];
+          }
+          if (qo.bias) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              x0[j] += bf2f(qo.bias[head * 128 + d0 + j]);
+              x1[j] += bf2f(qo.bias[head * 128 + d0 + 64 + j]);
+            }
+          }
+          if (head < qo.nh + qo.nkv) {
+            const f32x4* cs = (const f32x4*)(qo.rope + ((long)qo.row_pos[m] * 64 + d0) * 2);
+            const f32x4 a = cs[0], b = cs[1];  // (cos, sin) of dims d0, d0 + 1 and d0 + 2, d0 + 3
+            const float c[4] = {a[0], a[2], b[0], b[2]}, sn[4] = {a[1], a[3], b[1], b[3]};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const float y0 = x0[j] * c[j] - x1[j] * sn[j];
+              const float y1 = x1[j] * c[j] + x0[j] * sn[j];
+              x0[j] = y0;
+              x1[j] = y1;
+            }
+          }
+          uint16_t* dst;
+          if (head < qo.nh)
+            dst = qo.q + ((long)m * qo.nh + head) * 128;
+          else if (head < qo.nh + qo.nkv)
+            dst = qo.kc + ((long)(head - qo.nh) * qo.cache_rows + qo.row_tok[m]) * 128;
+          else
+            dst = qo.vc + ((long)(head - qo.nh - qo.nkv) * qo.cache_rows + qo.row_tok[m]) * 128;
+          u32x2 w0, w1;
+          w0.x = (uint32_t)f2bf(x0[0]) | ((uint32_t)f2bf(x0[1]) << 16);
+          w0.y = (uint32_t)f2bf(x0[2]) | ((uint32_t)f2bf(x0[3]) << 16);
+          w1.x = (uint32_t)f2bf(x1[0]) | ((uint32_t)f2bf(x1[1]) << 16);
+          w1.y = (uint32_t)f2bf(x1[2]) | ((uint32_t)f2bf(x1[3]) << 16);
+          *(u32x2*)(dst + d0) = w0;
+          *(u32x2*)(dst + d0 + 64) = w1;
+        }
+        continue;
+      }
+      if constexpr (EPI == kTileEpiSwiGlu) {
         const int F = N >> 1;
         const int i = nb * TNB + wn * NFW + ii;
 #pragma unroll
@@ -284,14 +342,14 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_bf16_dma(const uint16_t* __
 // 128 with the pinned schedule and 4 stages, in bands of 8 row tiles, beat 8
 // waves without bands: Q/K/V (12288 x 4096) 1042-1046 us against 1155, O
 // 325 against 323-428, down 997 against 1004-1172.
-template <bool SWIGLU>
+template <int EPI>
 static bool launch_dma(const GemmPlan& p, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
                        const uint16_t* X, int ldx, const u32x4* Wp, float* C, int M, int N,
-                       int K, int NB, int MT, int S, int ks, uint16_t* out) {
+                       int K, int NB, int MT, int S, int ks, uint16_t* out, const QkvOut& qo) {
   const dim3 grid(p.grid), b(64 * p.dma_nw);
 #define WD_DMA(MFW, ST, NW, TNB, SCH)                                                          \
-  launch_timed_block(k_gemm_bf16_dma<MFW, ST, SWIGLU, NW, TNB, SCH>, grid, b, st, e0, e1, X, ldx, \
-                     Wp, C, M, N, K, NB, MT, S, ks, p.dma_gm, out)
+  launch_timed_block(k_gemm_bf16_dma<MFW, ST, EPI, NW, TNB, SCH>, grid, b, st, e0, e1, X, ldx,  \
+                     Wp, C, M, N, K, NB, MT, S, ks, p.dma_gm, out, qo)
   if (p.dma_nw == 4 && p.dma_tnb == 8 && p.dma_mfw == 4) {
     WD_DMA(4, 4, 4, 8, 1);
     return true;
@@ -326,14 +384,19 @@ static bool launch_dma(const GemmPlan& p, hipStream_t st, hipEvent_t e0, hipEven
 
 bool launch_gemm_tiles(const GemmPlan& p, const uint16_t* X, int ldx, const void* Wp, float* C,
                        int M, int N, int K, uint16_t* swiglu_out, hipStream_t st, hipEvent_t e0,
-                       hipEvent_t e1) {
+                       hipEvent_t e1, const QkvOut* qkv) {
   const int TN = 32 * p.dma_tnb;
   const int NB = N / TN, MT = (M + 64 * p.dma_mfw - 1) / (64 * p.dma_mfw);
+  const QkvOut none{};
+  if (qkv)
+    return p.splits == 1 &&
+           launch_dma<kTileEpiQkv>(p, st, e0, e1, X, ldx, (const u32x4*)Wp, nullptr, M, N, K, NB,
+                                   MT, 1, K / 32, nullptr, *qkv);
   if (swiglu_out)
-    return launch_dma<true>(p, st, e0, e1, X, ldx, (const u32x4*)Wp, nullptr, M, N, K, NB, MT, 1,
-                            K / 32, swiglu_out);
-  return launch_dma<false>(p, st, e0, e1, X, ldx, (const u32x4*)Wp, C, M, N, K, NB, MT, p.splits,
-                           p.ks_per_split, nullptr);
+    return launch_dma<kTileEpiSwiGlu>(p, st, e0, e1, X, ldx, (const u32x4*)Wp, nullptr, M, N, K,
+                                      NB, MT, 1, K / 32, swiglu_out, none);
+  return launch_dma<kTileEpiPartial>(p, st, e0, e1, X, ldx, (const u32x4*)Wp, C, M, N, K, NB, MT,
+                                     p.splits, p.ks_per_split, nullptr, none);
 }
 
 }  // namespace wd

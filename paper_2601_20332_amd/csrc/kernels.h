@@ -33,12 +33,34 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8 = false, int max_splits = 1
 // workgroup).  gemm_bf16 and gemm_bf16_swiglu_dma reject plans for which
 // this is false.
 bool gemm_plan_ok(const GemmPlan& p, int M, int N, int K, bool w8, bool swiglu);
+// Where the Q/K/V projection's epilogue in the many-row kernel puts its
+// results (bf16 models, head_dim 128, weights packed kPackRopePair): bias
+// (null without), the RoPE table [position][64][cos, sin], each row's
+// position and K/V cache row, q [M][nh][128], and this layer's K and V cache
+// [nkv][cache_rows][128].
+struct QkvOut {
+  const uint16_t* bias;
+  const float* rope;
+  const int32_t* row_pos;
+  const int32_t* row_tok;
+  uint16_t* q;
+  uint16_t* kc;
+  uint16_t* vc;
+  long cache_rows;
+  int nh, nkv;
+};
 // The many-row kernel (gemm_tiles.hip) for plan p (p.dma_mfw > 0, checked by
-// gemm_plan_ok): split-K partials into C, or with swiglu_out the SwiGLU
-// epilogue (no K split).  False if the plan names no instance.
+// gemm_plan_ok): split-K partials into C; with swiglu_out the SwiGLU
+// epilogue; with qkv the Q/K/V epilogue (both need p.splits == 1).  False if
+// the plan names no instance or does not fit the epilogue.
 bool launch_gemm_tiles(const GemmPlan& p, const uint16_t* X, int ldx, const void* Wp, float* C,
                        int M, int N, int K, uint16_t* swiglu_out, hipStream_t st, hipEvent_t e0,
-                       hipEvent_t e1);
+                       hipEvent_t e1, const QkvOut* qkv = nullptr);
+// Many-row Q/K/V product with its epilogue in the kernel: p must be a
+// k_gemm_bf16_dma plan without a K split for (M, N, K), N = (nh + 2 nkv) 128.
+hipError_t gemm_bf16_qkv_tiles(const uint16_t* X, int ldx, const void* Wp, int M, int N, int K,
+                               const GemmPlan& p, const QkvOut& qo, hipStream_t st,
+                               hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // The kernel plan p launches (1 pipelined few-row kernel with K-split
 // partials, 2 the many-row LDS-pipelined kernel, 3 the split-K tiled kernel)
 // and its workgroup tile and waves.

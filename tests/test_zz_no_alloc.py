@@ -79,12 +79,19 @@ def test_noalloc_steps_equal_wd_step_twice_second_smaller():
         m.free()
 
 
+# one 4096-wide layer: the output projection writes split-K partials of at
+# least rows x 4096 x 4 bytes, whatever its split count
+WIDE = synth.ModelShape(n_layers=1, hidden=4096, n_heads=32, n_kv_heads=32, head_dim=128,
+                        ffn=4096, vocab=192 * 64, dtype=synth.DTYPE_BF16, rms_eps=1e-5,
+                        rope_theta=10000.0)
+
+
 def test_noalloc_refuses_what_does_not_fit_and_leaves_the_sequence_untouched():
-    m = gpu_model(synth.Weights(SHAPE, seed=17))
+    m = gpu_model(synth.Weights(WIDE, seed=5))
     try:
-        # the first refresh runs 4 x (3000 + 40) rows: its Q/K/V partials alone
-        # exceed the static scratch
-        prompts = synth.prompts(SHAPE, [3000] * 4)
+        # the first refresh runs 4 x (2000 + 40) rows: its O partials alone
+        # (8160 x 4096 x 4 bytes) exceed the 96 MiB static scratch
+        prompts = synth.prompts(WIDE, [2000] * 4)
         gen = wd.wd_prefill_prompt(m, prompts, 24, wd.window_config(8, 32, 4, 2))
         with pytest.raises(wd.WdError) as ei:
             wd.wd_step_noalloc(gen)
@@ -94,6 +101,10 @@ def test_noalloc_refuses_what_does_not_fit_and_leaves_the_sequence_untouched():
         assert r.step == 0 and r.is_refresh
         wd.wd_get_state(gen)
         gen.free()
+    finally:
+        m.free()
+    m = gpu_model(synth.Weights(SHAPE, seed=17))
+    try:
         # settings it does not take
         eos = wd.wd_prefill_prompt(m, synth.prompts(SHAPE, [20]), 8,
                                    wd.window_config(4, 4, 2, 1, eos_id=5))
