@@ -440,32 +440,61 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
   const int n_it = (KTs + U - 1) / U;
   u32x4 pre[XD][PER_T];
   u32x4 a[R][UW];
-  auto wload = [&](auto B, int it) {
+  // EV (the split's K steps a multiple of U, as at every shipped shape): one
+  // clamped iteration index per load group, the per-thread activation offsets
+  // computed once, and no zero masks when staging (rows past M repeat row
+  // M - 1, whose products are never stored).  Otherwise every load clamps its
+  // own K step and the staging zeroes rows past M and K steps past the end.
+  // Both give the same sums.
+  const u32x4* xrow[PER_T];
+#pragma unroll
+  for (int i = 0; i < PER_T; ++i) {
+    const int e = min(tid + i * NT, CHUNK16 - 1);
+    const int r = e / (U * 4), cc = e % (U * 4);
+    xrow[i] = (const u32x4*)(X + (long)min(r, M - 1) * ldx + (kt_begin + cc / 4) * 32 + (cc & 3) * 8);
+  }
+  auto wload = [&](auto B, int it, auto EV) {
     constexpr int b = decltype(B)::value;
+    if constexpr (decltype(EV)::value) {
+      const u32x4* base = wp + (long)min(it, n_it - 1) * (UW * 64);
 #pragma unroll
-    for (int u = 0; u < UW; ++u)
-      a[b][u] = __builtin_nontemporal_load(wp + (long)min(it * UW + u, frags - 1) * 64);
-  };
-  auto xload = [&](auto P, int it) {
-    constexpr int p = decltype(P)::value;
+      for (int u = 0; u < UW; ++u) a[b][u] = __builtin_nontemporal_load(base + u * 64);
+    } else {
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      const int e = min(tid + i * NT, CHUNK16 - 1);
-      const int r = e / (U * 4), cc = e % (U * 4);
-      const long row = min(r, M - 1);
-      const int kc = kt_begin + min(it * U + cc / 4, KTs - 1);
-      pre[p][i] = *(const u32x4*)(X + row * ldx + kc * 32 + (cc & 3) * 8);
+      for (int u = 0; u < UW; ++u)
+        a[b][u] = __builtin_nontemporal_load(wp + (long)min(it * UW + u, frags - 1) * 64);
     }
   };
-  auto xstore = [&](auto P, int buf, int it) {
+  auto xload = [&](auto P, int it, auto EV) {
+    constexpr int p = decltype(P)::value;
+    if constexpr (decltype(EV)::value) {
+      const long step = (long)min(it, n_it - 1) * (U * 4);  // u32x4 per iteration of a row
+#pragma unroll
+      for (int i = 0; i < PER_T; ++i) pre[p][i] = xrow[i][step];
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER_T; ++i) {
+        const int e = min(tid + i * NT, CHUNK16 - 1);
+        const int r = e / (U * 4), cc = e % (U * 4);
+        const long row = min(r, M - 1);
+        const int kc = kt_begin + min(it * U + cc / 4, KTs - 1);
+        pre[p][i] = *(const u32x4*)(X + row * ldx + kc * 32 + (cc & 3) * 8);
+      }
+    }
+  };
+  auto xstore = [&](auto P, int buf, int it, auto EV) {
     constexpr int p = decltype(P)::value;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
       const int e = tid + i * NT;
       if (CHUNK16 % NT == 0 || e < CHUNK16) {
         const int r = e / (U * 4), cc = e % (U * 4);
-        const bool ok = r < M && it * U + cc / 4 < KTs;
-        *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[p][i] : zero;
+        if constexpr (decltype(EV)::value) {
+          *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = pre[p][i];
+        } else {
+          const bool ok = r < M && it * U + cc / 4 < KTs;
+          *(u32x4*)(&xs[buf][r * PITCH + cc * 8]) = ok ? pre[p][i] : zero;
+        }
       }
     }
   };
@@ -493,12 +522,12 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
     }
   };
   // iteration it = base + J with base a multiple of R (and of XD): buffers are static
-  auto body = [&](auto J, int it) {
+  auto body = [&](auto J, int it, auto EV) {
     constexpr int j = decltype(J)::value;
-    xload(ic<j % XD>{}, it + XD);
-    wload(ic<(j + R - 1) % R>{}, it + R - 1);
+    xload(ic<j % XD>{}, it + XD, EV);
+    wload(ic<(j + R - 1) % R>{}, it + R - 1, EV);
     if (it < n_it) compute(ic<j % R>{}, j & 1);
-    xstore(ic<(j + 1) % XD>{}, (j + 1) & 1, it + 1);
+    xstore(ic<(j + 1) % XD>{}, (j + 1) & 1, it + 1, EV);
     __syncthreads();
   };
   // Q/K/V epilogue inputs, loaded before the K loop so that their latency
@@ -520,12 +549,18 @@ __global__ __launch_bounds__(64 * GW) void k_gemm_bf16_fused(const uint16_t* __r
       qkv_cs[jf][1] = cs[1];
     }
   }
-  static_for<0, XD>([&](auto J) { xload(J, decltype(J)::value); });
-  static_for<0, R - 1>([&](auto J) { wload(J, decltype(J)::value); });
-  xstore(ic<0>{}, 0, 0);
-  __syncthreads();
-  for (int it = 0; it < n_it; it += R)
-    static_for<0, R>([&](auto J) { body(J, it + decltype(J)::value); });
+  auto run = [&](auto EV) {
+    static_for<0, XD>([&](auto J) { xload(J, decltype(J)::value, EV); });
+    static_for<0, R - 1>([&](auto J) { wload(J, decltype(J)::value, EV); });
+    xstore(ic<0>{}, 0, 0, EV);
+    __syncthreads();
+    for (int it = 0; it < n_it; it += R)
+      static_for<0, R>([&](auto J) { body(J, it + decltype(J)::value, EV); });
+  };
+  if (KTs % U == 0)  // uniform over the grid
+    run(std::true_type{});
+  else
+    run(std::false_type{});
 
   // the confidence epilogue has barriers; its launches divide the groups evenly
   if constexpr (EPI != kEpiConf)
