@@ -664,11 +664,14 @@ __global__ __launch_bounds__(64 * NWQ) void k_attn_bf16_grouped(const uint16_t* 
   }
 }
 
-// out = sum_s exp(m_s - m) O_s / sum_s exp(m_s - m) l_s, m = max_s m_s
+// out = sum_s exp(m_s - m) O_s / sum_s exp(m_s - m) l_s, m = max_s m_s.
+// Workgroup (h, r) of the (nh, M) grid runs on the XCD (linear id mod 8) that
+// ran every split of head h when nh is a multiple of 8, so the partials it
+// reads were written through its own L2.
 __global__ __launch_bounds__(128) void k_attn_combine(const float* __restrict__ part,
                                                       const float* __restrict__ ml, int nsplit,
                                                       int M, int nh, uint16_t* __restrict__ o) {
-  const int r = blockIdx.x, h = blockIdx.y, dd = threadIdx.x;
+  const int h = blockIdx.x, r = blockIdx.y, dd = threadIdx.x;
   // every split's (m, l, O) in flight at once; nsplit <= kMaxSplit, and only
   // the splits that exist are loaded (nsplit is uniform, so are the branches)
   float ms[kMaxSplit], ls[kMaxSplit], os[kMaxSplit];
@@ -754,14 +757,14 @@ hipError_t attention_bf16(const uint16_t* q, const uint16_t* kcache, const uint1
                           kcache, vcache, cache_rows, o, g, n_heads, n_kv, nsplit, tps * kKT, M,
                           part, ml);
     if (nsplit > 1)
-      hipExtLaunchKernelGGL(k_attn_combine, dim3(M, n_heads), dim3(kAttD), 0, st, nullptr, e1, 0,
+      hipExtLaunchKernelGGL(k_attn_combine, dim3(n_heads, M), dim3(kAttD), 0, st, nullptr, e1, 0,
                             (const float*)part, (const float*)ml, nsplit, M, n_heads, o);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_attn_bf16, grid, dim3(256), 0, st, q, kcache, vcache, cache_rows, o, g,
                      n_heads, n_kv, nsplit, tps * kKT, M, part, ml);
   if (nsplit > 1)
-    hipLaunchKernelGGL(k_attn_combine, dim3(M, n_heads), dim3(kAttD), 0, st, part, ml, nsplit, M,
+    hipLaunchKernelGGL(k_attn_combine, dim3(n_heads, M), dim3(kAttD), 0, st, part, ml, nsplit, M,
                        n_heads, o);
   return hipGetLastError();
 }
