@@ -1119,6 +1119,14 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
       add(4);
       pick = best();
     }
+    // From four rounds of unsplit 256 x 256 tiles on (batched refresh steps),
+    // those tiles on the pinned 4-wave schedule beat the finer tiles the work
+    // count prefers, though they round up more rows: Q/K/V and gate/up at
+    // 3000-11000 rows 2-9% faster (gate/up at 5000 rows 922 against 1014 us,
+    // 192- or 128-row tiles); O and down reach four rounds only past 16000
+    // rows.  Every output sums K in the same order on either tile.
+    for (int i = 0; i < n; ++i)
+      if (c[i].mfw == 4 && c[i].tnb == 8 && c[i].splits == 1 && c[i].grid >= 1024) pick = &c[i];
     p.dma_mfw = pick->mfw;
     p.dma_tnb = pick->tnb;
     p.splits = pick->splits;

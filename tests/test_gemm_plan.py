@@ -92,6 +92,19 @@ def test_llada_refresh_rows_take_the_measured_tiles():
     assert _check(34, 4096, 12288, False)["kernel"] == 1
 
 
+def test_batched_refresh_rows_take_pinned_256_tiles():
+    # four or more rounds of unsplit 256 x 256 tiles: those tiles on the
+    # pinned 4-wave schedule, whatever the work count prefers
+    for M in (3000, 5000, 7000, 11000):
+        gu = _check(M, 24576, 4096, False)
+        assert (gu["rows"], gu["features"], gu["waves"], gu["splits"]) == (256, 256, 4, 1)
+    for M in (7000, 9000, 14000):
+        qkv = _check(M, 12288, 4096, False)
+        assert (qkv["rows"], qkv["features"], qkv["waves"], qkv["splits"]) == (256, 256, 4, 1)
+    # below four rounds the work count decides (Q/K/V at 3000 rows: 576 workgroups)
+    assert _check(3000, 12288, 4096, False)["waves"] != 4
+
+
 def test_invalid_arguments():
     with pytest.raises(wd.WdError):
         wd.wd_debug_gemm_plan(0, 256, 256)
