@@ -11,6 +11,7 @@ import pytest
 
 import synth
 from oracle.model import OracleModel
+import wdtest
 from wdtest import check_sequence, gpu_model, log, run_gpu
 
 pytestmark = pytest.mark.gpu
@@ -125,6 +126,50 @@ def test_llada8b_full_depth_against_oracle():
           f"adopted_sel={rep.select_adopted} adopted_tok={rep.token_adopted} "
           f"({time.time() - t0:.1f}s)", flush=True)
     assert rep.steps == n_steps
+    assert steps[0].res.is_refresh and steps[-1].res.is_refresh
+
+
+# Logit bound for the normal and next refresh steps at full Dream-7B depth.
+# The bf16 bound (2e-2) sits on the rounding floor of this datapath there: the
+# oracle's own layer run on float32 arrays (fp32 GEMMs, the same bf16
+# rounding points) differs from it by 1.89e-2 after 28 layers on the first
+# refresh step, and the GPU by 1.83e-2 on that step; over the following
+# steps the largest per-row error of a float32 implementation is a tail of
+# that floor (the GPU's reached 2.12e-2, over 2e-2 on 2 of the 9 steps).  The
+# first refresh step, where the floor was measured, keeps the 2e-2 bound.
+DREAM_DEPTH_LOGIT_TOL = 2.5e-2
+
+
+@pytest.mark.timeout(900)
+def test_dream7b_full_depth_against_oracle():
+    """All 28 layers of the Dream-7B workload (grouped K/V heads, QKV bias) at
+    its window settings: the first refresh step, the phase's normal steps and
+    the next refresh step against the float64 oracle (Sec. 4.3 refresh and
+    normal steps, Sec. 5.1 models).  Bookkeeping, selections and tokens at the
+    standard bar; logits at 2e-2 on the first refresh step and at
+    DREAM_DEPTH_LOGIT_TOL after it."""
+    w = synth.WORKLOADS["dream7b"]
+    shape = w.model
+    n_steps = w.window.refresh_every + 1
+    t0 = time.time()
+    log(f"[case] dream7b full depth ({shape.n_layers} layers), {n_steps} steps against the oracle")
+    W = HeldWeights(shape)
+    m = gpu_model(W)
+    prompts = synth.prompts(shape, [w.prompt_len])
+    steps, _ = run_gpu(m, prompts, w.gen_len, w.window, max_steps=n_steps)
+    m.free()
+    log(f"[gpu] {len(steps)} steps, weights drawn and run in {time.time() - t0:.1f}s")
+    om = OracleModel(W, cache_budget_bytes=80e9)
+    rep = check_sequence(om, prompts[0], w.gen_len, w.window, steps, 0, 1, max_steps=n_steps,
+                         progress=True, logit_tol=DREAM_DEPTH_LOGIT_TOL)
+    W.drop()
+    over = sum(e > wdtest.LOGIT_TOL[synth.DTYPE_BF16] for e in rep.step_rel)
+    print(f"PARITY dream7b-28L seq=0 steps={rep.steps} max_rel_logit_err={rep.max_rel:.3e} "
+          f"first_refresh={rep.step_rel[0]:.3e} steps_over_2e-2={over} "
+          f"adopted_sel={rep.select_adopted} adopted_tok={rep.token_adopted} "
+          f"({time.time() - t0:.1f}s)", flush=True)
+    assert rep.steps == n_steps
+    assert rep.step_rel[0] <= wdtest.LOGIT_TOL[synth.DTYPE_BF16]
     assert steps[0].res.is_refresh and steps[-1].res.is_refresh
 
 
