@@ -58,47 +58,60 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// Sum over the block (blockDim.x a multiple of 64, <= 1024); every thread gets
-// the total.  The summation order is fixed, so results are reproducible.
 // Sum of p[s * stride] for s = 0..S-1, added in order of s.  Loads go out
-// eight at a time from clamped addresses, so a wave waits for one round trip
-// per eight partials rather than one per partial; the out-of-range lanes of
-// the last batch add zero.
-template <typename V>
-__device__ __forceinline__ V split_sum(const V* __restrict__ p, long stride, int S) {
+// in batches from clamped addresses, so a wave waits for one round trip per
+// batch rather than one per partial; the out-of-range lanes of the last batch
+// add zero.  Batches of 4 when S <= 4 (the few-row split-K products), else 8:
+// no load is issued for a partial that does not exist up to 4.
+template <int NB, typename V>
+__device__ __forceinline__ V split_sum_nb(const V* __restrict__ p, long stride, int S) {
   V acc{};
-  for (int s0 = 0; s0 < S; s0 += 8) {
-    V t[8];
+  for (int s0 = 0; s0 < S; s0 += NB) {
+    V t[NB];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) t[j] = p[(long)min(s0 + j, S - 1) * stride];
+    for (int j = 0; j < NB; ++j) t[j] = p[(long)min(s0 + j, S - 1) * stride];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc += s0 + j < S ? t[j] : V{};
+    for (int j = 0; j < NB; ++j) acc += s0 + j < S ? t[j] : V{};
   }
   return acc;
 }
+template <typename V>
+__device__ __forceinline__ V split_sum(const V* __restrict__ p, long stride, int S) {
+  return S <= 4 ? split_sum_nb<4>(p, stride, S) : split_sum_nb<8>(p, stride, S);
+}
 
 // Two such sums over the same split index with their loads interleaved.
-template <typename V>
-__device__ __forceinline__ void split_sum2(const V* __restrict__ p, const V* __restrict__ q,
-                                           long stride, int S, V& a, V& b) {
+template <int NB, typename V>
+__device__ __forceinline__ void split_sum2_nb(const V* __restrict__ p, const V* __restrict__ q,
+                                              long stride, int S, V& a, V& b) {
   a = V{};
   b = V{};
-  for (int s0 = 0; s0 < S; s0 += 8) {
-    V t[8], u[8];
+  for (int s0 = 0; s0 < S; s0 += NB) {
+    V t[NB], u[NB];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < NB; ++j) {
       const long o = (long)min(s0 + j, S - 1) * stride;
       t[j] = p[o];
       u[j] = q[o];
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < NB; ++j) {
       a += s0 + j < S ? t[j] : V{};
       b += s0 + j < S ? u[j] : V{};
     }
   }
 }
+template <typename V>
+__device__ __forceinline__ void split_sum2(const V* __restrict__ p, const V* __restrict__ q,
+                                           long stride, int S, V& a, V& b) {
+  if (S <= 4)
+    split_sum2_nb<4>(p, q, stride, S, a, b);
+  else
+    split_sum2_nb<8>(p, q, stride, S, a, b);
+}
 
+// Sum over the block (blockDim.x a multiple of 64, <= 1024); every thread gets
+// the total.  The summation order is fixed, so results are reproducible.
 __device__ __forceinline__ float block_sum(float v, float* red /* >= 16 floats of LDS */) {
   v = wave_sum(v);
   const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
