@@ -1025,7 +1025,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_big(const uint16_t* __rest
 GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
   GemmPlan p;
   const int KT = K / 32;
-  if (M <= 96 && !w8 && K >= N && N % 64 == 0) {
+  if (M <= 96 && !w8 && (K >= N || (N / 64 < 192 && M <= 64)) && N % 64 == 0) {
     // K at least N (O, down): the pipelined kernel with partials, 4 groups
     // per workgroup and the most power-of-two splits that keep one round of
     // workgroups, each split at least 16 K steps (measured with weights read
@@ -1037,10 +1037,15 @@ GemmPlan plan_gemm_bf16(int M, int N, int K, bool w8, int max_splits) {
     // Where 4 groups per workgroup cannot fill the CUs (Dream-7B's 3584-wide
     // O and down: 224 workgroups), 7 groups with twice the splits may: the
     // fullest one-round grid wins, ties to fewer splits.
+    // Products too narrow for the fused kernel (N / 64 < 192) take this one
+    // too up to 64 rows, whatever K: Dream-7B's Q/K/V (4608 x 3584) with 3 groups per
+    // workgroup and 2 splits runs 10.2-10.8 us against 10.3-10.9 for the
+    // kernel below with 8 splits, and the Q/K/V epilogue reads 2 partials
+    // instead of 8.
     const int groups = N / 16;
     int best_gw = 4, best_S = 1;
     long best_grid = -1;
-    for (int gw : {4, 7}) {
+    for (int gw : {4, 7, 3}) {
       if (groups % gw) continue;
       int S = 1;
       while (2 * S <= max_splits && (long)(groups / gw) * 2 * S <= 256 && KT / (2 * S) >= 16) S *= 2;

@@ -135,7 +135,7 @@ def test_llada8b_full_depth_against_oracle():
 # rounding points) differs from it by 1.89e-2 after 28 layers on the first
 # refresh step, and the GPU by 1.83e-2 on that step; over the following
 # steps the largest per-row error of a float32 implementation is a tail of
-# that floor (the GPU's reached 2.12e-2, over 2e-2 on 2 of the 9 steps).  The
+# that floor (the GPU's reached 2.11-2.12e-2, over 2e-2 on 1-2 of 9 steps).  The
 # first refresh step, where the floor was measured, keeps the 2e-2 bound.
 DREAM_DEPTH_LOGIT_TOL = 2.5e-2
 
