@@ -105,6 +105,20 @@ def test_batched_refresh_rows_take_pinned_256_tiles():
     assert _check(3000, 12288, 4096, False)["waves"] != 4
 
 
+def test_narrow_products_take_the_pipelined_split_kernel():
+    # Q/K/V of Dream-7B (4608 x 3584) is too narrow for the fused epilogue
+    # kernel: up to 64 rows it runs the pipelined split kernel with 3 groups per
+    # workgroup and 2 splits (so the Q/K/V epilogue reads 2 partials)
+    for M in (34, 40, 46, 64):
+        p = _check(M, 4608, 3584, False)
+        assert (p["kernel"], p["waves"], p["splits"]) == (1, 3, 2), p
+    # above 64 rows the many-row tiles keep it
+    assert _check(80, 4608, 3584, False)["kernel"] == 2
+    # wide products keep their plans (LLaDA-8B Q/K/V at normal-step rows is fused,
+    # not planned here; O and down stay on 4 groups per workgroup)
+    assert _check(39, 4096, 4096, False)["waves"] == 4
+
+
 def test_invalid_arguments():
     with pytest.raises(wd.WdError):
         wd.wd_debug_gemm_plan(0, 256, 256)
